@@ -1,0 +1,233 @@
+"""Throughput of one DiT denoising step on one MI355X.
+
+A step is the whole hot path over one batch of synthetic input: timestep
+embedding and all adaLN modulation vectors, the input embedders, 19
+double-stream and 38 single-stream blocks (adaLN LayerNorm, QKV + 2-D RoPE,
+joint attention, gated MLP, gated residuals), the final layer and the
+flow-matching Euler update -- dit_step followed by euler_update.
+
+Default workload: the 1024 px request (4096 image + 512 text tokens) of the
+FLUX.1-dev-shaped model, bf16 weights with fp32 accumulation.  Weights and
+inputs are seeded random values drawn on the GPU (no trained checkpoint).
+Prints one JSON line on stdout; progress goes to stderr.
+
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--extra A,B]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "DiT denoising steps/sec per resolution; attention+GEMM TFLOP/s and % bf16 peak"
+BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+F32_PEAK_TFLOPS = 157.3
+HBM_PEAK_GBS = 8000.0
+
+
+def log(msg: str) -> None:
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def make_model(torch, dit, synth, m, seed, dev):
+    cfg = dit.make_config(m)
+    shapes = dit.weight_manifest(cfg)
+    dt = torch.bfloat16 if m.dtype == "bf16" else torch.float32
+    tensors = [synth.device_normal(seed, "w:" + n, s, synth.WEIGHT_STD, dt, dev) for n, s in shapes]
+    return cfg, dit.Weights(tensors)
+
+
+def run_workload(torch, dit, synth, workloads, wl, cfg, w, steps, warmup, seed, dev, profile=True):
+    m = wl.model
+    dt_t = torch.bfloat16 if m.dtype == "bf16" else torch.float32
+    grids = wl.grids()
+    n_img = wl.n_img()
+    import numpy as np
+    if wl.t is None:
+        ts = [float(x) for x in synth.uniform(seed, "timesteps:" + wl.name, (len(grids),))]
+    else:
+        ts = list(wl.t)
+    b = dit.Batch(grids, grids, wl.n_txt, ts)
+    nws = dit.workspace_size(cfg, b)
+    ws = torch.empty(nws, dtype=torch.uint8, device=dev)
+    lat = synth.device_normal(seed, "latents:" + wl.name, (sum(n_img), m.in_channels), 1.0, dt_t, dev)
+    txt = synth.device_normal(seed, "text:" + wl.name, (sum(wl.n_txt), m.text_dim), 1.0, dt_t, dev)
+    vel = torch.empty_like(lat)
+    dts = [wl.dt] * len(grids)
+    stream = torch.cuda.current_stream()
+    dtype = dit.DIT_BF16 if m.dtype == "bf16" else dit.DIT_F32
+
+    def step():
+        dit.dit_step(cfg, w, b, lat, txt, vel, ws, nws, stream)
+        dit.euler_update(b, m.in_channels, dtype, lat, vel, dts, stream)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev[0].record(stream)
+    for i in range(steps):
+        step()
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+    assert torch.isfinite(vel.float()).all().item(), "non-finite velocity"
+    kernels = None
+    if profile:
+        dit.profile_start()
+        for _ in range(max(1, min(steps, 3))):
+            step()
+        torch.cuda.synchronize()
+        kernels = dit.profile_stop()
+        nprof = max(1, min(steps, 3))
+        for k in kernels.values():
+            k["launches"] //= 1
+            k["ms_per_step"] = k["ms"] / nprof
+    flops = workloads.flops_per_step(m, wl.n_txt, n_img)
+    ms = wall * 1000.0 / steps
+    res = {
+        "steps_per_s": steps / wall, "ms_per_step": ms, "ms_median_event": statistics.median(per),
+        "cv_pct": 100.0 * statistics.pstdev(per) / statistics.mean(per),
+        "tflop_per_step": flops["total"] / 1e12, "tflops": flops["total"] / (ms / 1e3) / 1e12,
+        "gemm_tflop": flops["gemm"] / 1e12, "attention_tflop": flops["attention"] / 1e12,
+        "kernels": kernels,
+    }
+    peak = BF16_PEAK_TFLOPS if m.dtype == "bf16" else F32_PEAK_TFLOPS
+    res["frac_peak"] = res["tflops"] / peak
+    del ws, lat, txt, vel
+    return res
+
+
+def roofline(kernels, dtype: str):
+    """Dominant kernel family by time: algorithmic work per launch over its
+    average launch duration (HIP events on the launch stream)."""
+    name, k = max(kernels.items(), key=lambda kv: kv[1]["ms"])
+    avg_ms = k["ms"] / k["launches"]
+    if k["flops"] > 0:
+        peak = BF16_PEAK_TFLOPS if dtype == "bf16" else F32_PEAK_TFLOPS
+        ach = k["flops"] / k["launches"] / (avg_ms / 1e3) / 1e12
+        return {"kernel": name, "bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s",
+                "frac": ach / peak, "traffic": None, "launches_per_step": None, "avg_launch_ms": avg_ms,
+                "flop_per_launch": k["flops"] / k["launches"]}
+    ach = k["bytes"] / k["launches"] / (avg_ms / 1e3) / 1e9
+    return {"kernel": name, "bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": ach / HBM_PEAK_GBS, "traffic": None, "avg_launch_ms": avg_ms,
+            "bytes_per_launch": k["bytes"] / k["launches"]}
+
+
+def cpu_baseline(wl, seed: int):
+    """The oracle (fp64, as it stands) on a bounded sample of the workload:
+    one double-stream and one single-stream block at the workload's token
+    counts, extrapolated to the model's block counts."""
+    import numpy as np
+    import oracle as O
+    from paper_2510_01565_amd import synth
+    m = wl.model
+    threads = None
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((i.get("num_threads") or 0) for i in threadpool_info()) or None
+    except Exception:
+        pass
+    cfg1 = O.OracleConfig(hidden=m.hidden, heads=m.heads, head_dim=m.head_dim, mlp_ratio=m.mlp_ratio, n_double=1,
+                          n_single=1, in_channels=m.in_channels, text_dim=m.text_dim)
+    shapes = [(n, s) for n, s in O.param_shapes(cfg1) if n.startswith(("double.", "single.", "mod."))]
+    params = synth.make_params(shapes, seed, bf16=True)
+    H = m.hidden
+    gh = wl.grids()[0]
+    nt = wl.n_txt[0]
+    xt = synth.normal(seed, "cpu.txt", (nt, H), bf16=True).astype(np.float64)
+    xi = synth.normal(seed, "cpu.img", (gh * gh, H), bf16=True).astype(np.float64)
+    c = synth.normal(seed, "cpu.c", (H,)).astype(np.float64)
+    p64 = {k: v.astype(np.float64) for k, v in params.items()}
+    t0 = time.perf_counter()
+    yt, yi = O.double_block(p64, cfg1, 0, xt, xi, c, (gh, gh))
+    t_d = time.perf_counter() - t0
+    x = np.concatenate([yt, yi])
+    t0 = time.perf_counter()
+    O.single_block(p64, cfg1, 0, x, nt, c, (gh, gh))
+    t_s = time.perf_counter() - t0
+    t_step = m.n_double * t_d + m.n_single * t_s
+    return {"value": 1.0 / t_step, "unit": "steps/s", "cores": threads or os.cpu_count(), "kind": "oracle",
+            "sample": f"oracle (numpy fp64) on one double-stream ({t_d:.2f} s) and one single-stream block "
+                      f"({t_s:.2f} s) at {nt} text + {gh * gh} image tokens, extrapolated to "
+                      f"{m.n_double} + {m.n_single} blocks ({t_step:.1f} s per step)",
+            "s_per_step": t_step}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="dit57_1024px_bf16")
+    ap.add_argument("--extra", default="dit57_2048px_bf16,dit57_packed_mixed_bf16",
+                    help="comma-separated further workloads reported per resolution ('' for none)")
+    ap.add_argument("--extra-steps", type=int, default=3)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported by this build "
+              "(the step is measured on one GPU's share, see the design notes on sharding)", file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2510_01565_amd import dit, synth, workloads
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    dit.lib()
+    wl = workloads.WORKLOADS[args.workload]
+    log(f"workload {wl.name}: {wl.note}")
+    t0 = time.perf_counter()
+    cfg, w = make_model(torch, dit, synth, wl.model, args.seed, dev)
+    torch.cuda.synchronize()
+    log(f"weights drawn on the GPU in {time.perf_counter() - t0:.1f} s")
+    main_res = run_workload(torch, dit, synth, workloads, wl, cfg, w, args.steps, args.warmup, args.seed, dev)
+    log(f"{wl.name}: {main_res['ms_per_step']:.2f} ms/step, {main_res['tflops']:.1f} TFLOP/s "
+        f"({100 * main_res['frac_peak']:.1f}% of peak), CV {main_res['cv_pct']:.2f}%")
+    per = {wl.name: {k: v for k, v in main_res.items() if k != "kernels"}}
+    for name in [x for x in args.extra.split(",") if x]:
+        ow = workloads.WORKLOADS[name]
+        if ow.model != wl.model or ow.kind != "step":
+            continue
+        r = run_workload(torch, dit, synth, workloads, ow, cfg, w, args.extra_steps, 1, args.seed, dev,
+                         profile=False)
+        log(f"{name}: {r['ms_per_step']:.2f} ms/step, {r['tflops']:.1f} TFLOP/s ({100 * r['frac_peak']:.1f}% of peak)")
+        per[name] = {k: v for k, v in r.items() if k != "kernels"}
+
+    rl = roofline(main_res["kernels"], wl.model.dtype)
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        cpu = cpu_baseline(wl, args.seed)
+        log(f"cpu baseline: {cpu['sample']}")
+    g = wl.grids()
+    out = {
+        "metric": METRIC, "value": main_res["steps_per_s"], "unit": "steps/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": main_res["ms_per_step"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": wl.model.dtype, "data": "synthetic (seeded random weights and inputs)",
+        "config": {"workload": wl.name, "resolution_px": wl.resolutions, "image_tokens": wl.n_img(),
+                   "text_tokens": wl.n_txt, "requests": len(g), "parallelism": "single GPU"},
+        "tflops": main_res["tflops"], "frac_bf16_peak": main_res["frac_peak"],
+        "tflop_per_step": main_res["tflop_per_step"], "cv_pct": main_res["cv_pct"],
+        "roofline": rl, "cpu_baseline": cpu, "per_workload": per,
+        "kernels_ms_per_step": {k: round(v["ms_per_step"], 4) for k, v in main_res["kernels"].items()},
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,330 @@
+// Joint text+image attention, O = softmax(Q K^T / sqrt(d)) V per head and per
+// request, never materialising the L x L score matrix (online softmax over
+// 64-key tiles).
+//
+// bf16 kernel (head_dim 128) on the gfx950 matrix cores.  Each wavefront owns
+// 32 queries.  It computes the transposed score tile S^T = K Q^T with
+// v_mfma_f32_32x32x16_bf16, so every lane holds the scores of ONE query
+// (column lane % 32) for half of the keys: the row max and row sum are
+// register reductions plus one exchange with lane ^ 32, no LDS.  The
+// probabilities are rounded to bf16 and fed straight from registers as the B
+// operand of O^T = V^T P^T; for that V is kept transposed (V^T [d][keys]) and
+// its 16-key groups are stored in LDS in the order the score registers hold
+// them.  K and V^T tiles are double-buffered in LDS (XOR-swizzled 16-byte
+// chunks); the softmax runs in the log2 domain (exp2 with log2(e)/sqrt(d)
+// folded into the scale).  Blocks of one head are mapped onto one XCD so its
+// K/V tiles are shared through that XCD's L2.
+#include <math.h>
+
+#include "device_common.h"
+
+namespace dit {
+
+namespace {
+
+// q-tiles of every request of the batch, longest requests first
+struct AttnSched {
+  int n;                     // number of requests with tokens
+  int req[kMaxReq];
+  int tile_off[kMaxReq + 1]; // prefix sum of q-tiles per head
+};
+
+constexpr int BQ = 128;  // queries per block (4 waves x 32)
+constexpr int BKV = 64;  // keys per tile
+constexpr int D = 128;
+
+__global__ __launch_bounds__(256) void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
+  __shared__ uint4 Ks[2][BKV * 16];  // [key][16 chunks of 8 d]
+  __shared__ uint4 Vs[2][D * 8];     // [d][8 chunks of 8 key slots]
+
+  const int per_head = sc.tile_off[sc.n];
+  const int id = xcd_remap(blockIdx.x, gridDim.x);
+  const int h = id / per_head;
+  const int t = id - h * per_head;
+  int slot = 0;
+  while (slot + 1 < sc.n && t >= sc.tile_off[slot + 1]) ++slot;
+  const int r = sc.req[slot];
+  const int q0 = (t - sc.tile_off[slot]) * BQ;
+  const int L = a.meta.joint_off[r + 1] - a.meta.joint_off[r];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int hl = lane >> 5;  // lane half
+
+  const bf16_t* __restrict__ Qg = (const bf16_t*)a.q + (long)a.qk_off[r] * a.q_tok + (long)h * a.q_head;
+  const bf16_t* __restrict__ Kg = (const bf16_t*)a.k + (long)a.qk_off[r] * a.k_tok + (long)h * a.k_head;
+  const bf16_t* __restrict__ Vg = (const bf16_t*)a.vt + (long)a.vt_off[r] + (long)h * a.vt_head;
+
+  // Q fragments (B operand of S^T = K Q^T): query q0 + wave*32 + lane%32, d chunk 2*ks + lane/32
+  const int qrow = q0 + wave * 32 + (lane & 31);
+  bf16x8_t qf[D / 16];
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) {
+    uint4 u = make_uint4(0, 0, 0, 0);
+    if (qrow < L) u = *(const uint4*)(Qg + (long)qrow * a.q_tok + (ks * 2 + hl) * 8);
+    qf[ks] = __builtin_bit_cast(bf16x8_t, u);
+  }
+
+  f32x16_t o[D / 32];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
+  float m_i = -INFINITY, l_i = 0.f;
+  const float sl2 = a.scale * 1.4426950408889634f;
+
+  uint4 rk[4], rv[4];
+  auto gload = [&](int kv0) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int idx = tid + c * 256;
+      const int row = idx >> 4, ch = idx & 15;
+      uint4 u = make_uint4(0, 0, 0, 0);
+      if (kv0 + row < L) u = *(const uint4*)(Kg + (long)(kv0 + row) * a.k_tok + ch * 8);
+      rk[c] = u;
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int idx = tid + c * 256;
+      const int dr = idx >> 3, ch = idx & 7;
+      const int key0 = kv0 + ch * 8;
+      // padded V^T: the 8 columns are inside the buffer; columns >= L are zeroed
+      uint4 u = *(const uint4*)(Vg + (long)dr * a.vt_d + key0);
+      if (key0 + 8 > L) {
+        uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (key0 + e >= L) w[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+        u = make_uint4(w[0], w[1], w[2], w[3]);
+      }
+      rv[c] = u;
+    }
+  };
+  auto lstore = [&](int st) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int idx = tid + c * 256;
+      const int row = idx >> 4, ch = idx & 15;
+      Ks[st][row * 16 + (ch ^ (row & 7))] = rk[c];
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int idx = tid + c * 256;
+      const int dr = idx >> 3, ch = idx & 7;
+      // keys 8*ch .. 8*ch+7 = 16-key group g, half hf; slot order inside a group is
+      // [0-3, 8-11, 4-7, 12-15] so lane half j reads its 8 keys as one 16-byte chunk
+      const int g = ch >> 1, hf = ch & 1;
+      uint2* row2 = (uint2*)&Vs[st][dr * 8];
+      const int u_lo = g * 4 + hf, u_hi = g * 4 + 2 + hf;  // 8-byte units
+      row2[(((u_lo >> 1) ^ (dr & 7)) << 1) | (u_lo & 1)] = make_uint2(rv[c].x, rv[c].y);
+      row2[(((u_hi >> 1) ^ (dr & 7)) << 1) | (u_hi & 1)] = make_uint2(rv[c].z, rv[c].w);
+    }
+  };
+
+  const int ntiles = (L + BKV - 1) / BKV;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+
+  for (int it = 0; it < ntiles; ++it) {
+    const int st = it & 1;
+    const int kv0 = it * BKV;
+    if (it + 1 < ntiles) gload(kv0 + BKV);
+
+    // S^T for 64 keys x 32 queries: two 32x32 blocks
+    f32x16_t s[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) s[kb][i] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const int key = kb * 32 + (lane & 31);
+        const uint4 u = Ks[st][key * 16 + ((ks * 2 + hl) ^ (key & 7))];
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, u), qf[ks], s[kb], 0, 0, 0);
+      }
+    }
+    if (kv0 + BKV > L) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int key = kv0 + kb * 32 + (i >> 2) * 8 + hl * 4 + (i & 3);
+          if (key >= L) s[kb][i] = -INFINITY;
+        }
+    }
+    float mx = s[0][0];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kb][i]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float m_new = fmaxf(m_i, mx * sl2);
+    const float alpha = exp2f(m_i - m_new);
+    m_i = m_new;
+
+    float ls = 0.f;
+    bf16x8_t pf[4];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float p = exp2f(fmaf(s[kb][i], sl2, -m_new));
+        ls += p;
+        pf[kb * 2 + (i >> 3)][i & 7] = (__bf16)p;
+      }
+    l_i = l_i * alpha + ls;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
+
+#pragma unroll
+    for (int ks2 = 0; ks2 < 4; ++ks2) {
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) {
+        const int dr = db * 32 + (lane & 31);
+        const uint4 u = Vs[st][dr * 8 + ((ks2 * 2 + hl) ^ (dr & 7))];
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, u), pf[ks2], o[db], 0, 0, 0);
+      }
+    }
+    if (it + 1 < ntiles) lstore(st ^ 1);
+    __syncthreads();
+  }
+
+  const float l = l_i + __shfl_xor(l_i, 32, 64);
+  if (qrow < L) {
+    const float inv = 1.0f / l;
+    const int p = a.meta.joint_off[r] + qrow;
+    const int row = a.o_stream_major ? joint_to_row(a.meta, p) : p;
+    bf16_t* og = (bf16_t*)a.o + (long)row * a.o_tok + (long)h * a.o_head;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int dd = db * 32 + g * 8 + hl * 4;
+        uint2 w;
+        w.x = pack_bf16x2(o[db][g * 4 + 0] * inv, o[db][g * 4 + 1] * inv);
+        w.y = pack_bf16x2(o[db][g * 4 + 2] * inv, o[db][g * 4 + 3] * inv);
+        *(uint2*)(og + dd) = w;
+      }
+  }
+}
+
+// ----------------------------------------------------------------------------
+// fp32 attention (head_dim 64) for fp32 models: one thread per query, K and V
+// tiles of 64 keys in LDS, online softmax in fp32 with expf.
+constexpr int FD = 64;
+constexpr int FQ = 64;
+
+__global__ __launch_bounds__(64) void attn_f32_kernel(const AttnArgs a, const AttnSched sc) {
+  __shared__ float Ksh[64][FD + 1];
+  __shared__ float Vsh[64][FD + 1];
+  const int per_head = sc.tile_off[sc.n];
+  const int h = blockIdx.x / per_head;
+  const int t = blockIdx.x - h * per_head;
+  int slot = 0;
+  while (slot + 1 < sc.n && t >= sc.tile_off[slot + 1]) ++slot;
+  const int r = sc.req[slot];
+  const int q0 = (t - sc.tile_off[slot]) * FQ;
+  const int L = a.meta.joint_off[r + 1] - a.meta.joint_off[r];
+  const int tid = threadIdx.x;
+  const int qrow = q0 + tid;
+
+  const float* Qg = (const float*)a.q + (long)a.qk_off[r] * a.q_tok + (long)h * a.q_head;
+  const float* Kg = (const float*)a.k + (long)a.qk_off[r] * a.k_tok + (long)h * a.k_head;
+  const float* Vg = (const float*)a.vt + (long)a.vt_off[r] + (long)h * a.vt_head;
+
+  float q[FD], o[FD];
+#pragma unroll
+  for (int c = 0; c < FD; ++c) {
+    q[c] = (qrow < L) ? Qg[(long)qrow * a.q_tok + c] : 0.f;
+    o[c] = 0.f;
+  }
+  float m = -INFINITY, l = 0.f;
+  for (int kv0 = 0; kv0 < L; kv0 += 64) {
+    __syncthreads();
+    for (int idx = tid; idx < 64 * FD; idx += 64) {
+      const int kr = idx / FD, c = idx % FD;
+      const bool ok = kv0 + kr < L;
+      Ksh[kr][c] = ok ? Kg[(long)(kv0 + kr) * a.k_tok + c] : 0.f;
+    }
+    for (int idx = tid; idx < 64 * FD; idx += 64) {
+      const int c = idx / 64, kr = idx % 64;
+      const bool ok = kv0 + kr < L;
+      Vsh[kr][c] = ok ? Vg[(long)c * a.vt_d + kv0 + kr] : 0.f;
+    }
+    __syncthreads();
+    const int nk = min(64, L - kv0);
+    for (int j = 0; j < nk; ++j) {
+      float sdot = 0.f;
+#pragma unroll
+      for (int c = 0; c < FD; ++c) sdot = fmaf(q[c], Ksh[j][c], sdot);
+      const float sc_ = sdot * a.scale;
+      const float mn = fmaxf(m, sc_);
+      const float al = expf(m - mn);
+      const float p = expf(sc_ - mn);
+      l = l * al + p;
+#pragma unroll
+      for (int c = 0; c < FD; ++c) o[c] = fmaf(p, Vsh[j][c], o[c] * al);
+      m = mn;
+    }
+  }
+  if (qrow < L) {
+    const int p = a.meta.joint_off[r] + qrow;
+    const int row = a.o_stream_major ? joint_to_row(a.meta, p) : p;
+    float* og = (float*)a.o + (long)row * a.o_tok + (long)h * a.o_head;
+    const float inv = 1.0f / l;
+#pragma unroll
+    for (int c = 0; c < FD; ++c) og[c] = o[c] * inv;
+  }
+}
+
+AttnSched make_sched(const BatchMeta& m, int bq) {
+  AttnSched sc{};
+  int order[kMaxReq];
+  int n = 0;
+  for (int r = 0; r < m.n_req; ++r)
+    if (m.joint_off[r + 1] > m.joint_off[r]) order[n++] = r;
+  // longest requests first: their tiles take longest, start them early
+  for (int i = 1; i < n; ++i)
+    for (int j = i; j > 0; --j) {
+      const int a = order[j - 1], b = order[j];
+      if (m.joint_off[b + 1] - m.joint_off[b] > m.joint_off[a + 1] - m.joint_off[a]) {
+        order[j - 1] = b;
+        order[j] = a;
+      }
+    }
+  sc.n = n;
+  sc.tile_off[0] = 0;
+  for (int i = 0; i < n; ++i) {
+    const int r = order[i];
+    sc.req[i] = r;
+    const int L = m.joint_off[r + 1] - m.joint_off[r];
+    sc.tile_off[i + 1] = sc.tile_off[i] + (L + bq - 1) / bq;
+  }
+  return sc;
+}
+
+}  // namespace
+
+hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s) {
+  if (a.head_dim != D) return hipErrorInvalidValue;
+  const AttnSched sc = make_sched(a.meta, BQ);
+  const long blocks = (long)sc.tile_off[sc.n] * a.heads;
+  if (blocks == 0) return hipSuccess;
+  hipLaunchKernelGGL(attn_bf16_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a, sc);
+  return hipGetLastError();
+}
+
+hipError_t launch_attention_f32(const AttnArgs& a, hipStream_t s) {
+  if (a.head_dim != FD) return hipErrorInvalidValue;
+  const AttnSched sc = make_sched(a.meta, FQ);
+  const long blocks = (long)sc.tile_off[sc.n] * a.heads;
+  if (blocks == 0) return hipSuccess;
+  hipLaunchKernelGGL(attn_f32_kernel, dim3((unsigned)blocks), dim3(64), 0, s, a, sc);
+  return hipGetLastError();
+}
+
+}  // namespace dit

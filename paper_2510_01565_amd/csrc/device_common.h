@@ -1,0 +1,116 @@
+// Device helpers for gfx950: bf16 storage conversions, wave64 reductions,
+// activations and the per-element GEMM epilogue.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dit_internal.h"
+
+namespace dit {
+
+typedef uint16_t bf16_t;  // raw bfloat16 storage
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf2f(bf16_t u) { return __uint_as_float(((uint32_t)u) << 16); }
+
+// fp32 -> bf16, round to nearest even (hardware conversion on gfx950)
+__device__ __forceinline__ bf16_t f2bf(float f) {
+  __bf16 b = (__bf16)f;
+  return __builtin_bit_cast(bf16_t, b);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+}
+
+template <typename T> __device__ __forceinline__ float to_f32(T v);
+template <> __device__ __forceinline__ float to_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ float to_f32<bf16_t>(bf16_t v) { return bf2f(v); }
+
+template <typename T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) { return f2bf(v); }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// GELU, tanh form: 0.5 x (1 + tanh(u)) = x * sigmoid(2u), u = sqrt(2/pi) (x + 0.044715 x^3)
+__device__ __forceinline__ float gelu_tanh(float x) {
+  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
+  float u = k0 * (x + 0.044715f * x * x * x);
+  return x / (1.0f + __expf(-2.0f * u));
+}
+
+__device__ __forceinline__ float silu(float x) { return x / (1.0f + __expf(-x)); }
+
+// One output element of a GEMM epilogue.  `y` already includes the bias;
+// `y_pair` is the value of the partner column n ^ 1 (RoPE pairs), bias included.
+template <typename T>
+__device__ __forceinline__ void epilogue_element(const EpiArgs& e, const BatchMeta& meta, int m, int n,
+                                                 float y, float y_pair) {
+  switch (e.mode) {
+    case EPI_STORE_F32:
+      ((float*)e.out)[(long)m * e.ldo + n] = y;
+      break;
+    case EPI_STORE_T:
+      ((T*)e.out)[(long)m * e.ldo + n] = from_f32<T>(y);
+      break;
+    case EPI_GELU:
+      ((T*)e.out)[(long)m * e.ldo + e.col0 + n] = from_f32<T>(gelu_tanh(y));
+      break;
+    case EPI_RESID: {
+      RowInfo ri = row_info(meta, e.row_base + m);
+      float g = e.mods[(long)ri.req * e.mods_ld + e.gate_off + n];
+      float* xo = (float*)e.out + (long)m * e.ldo + n;
+      *xo = *xo + g * y;
+      break;
+    }
+    case EPI_QKV: {
+      if (n >= e.n_qkv) {
+        ((T*)e.gelu_out)[(long)m * e.gelu_ld + e.gelu_col0 + (n - e.n_qkv)] = from_f32<T>(gelu_tanh(y));
+        break;
+      }
+      const int H = e.hidden, d = e.head_dim;
+      const int which = n / H;
+      const int hn = n - which * H;
+      const int h = hn / d, dd = hn - h * d;
+      RowInfo ri = row_info(meta, e.row_base + m);
+      const int p = padded_pos(meta, ri);
+      float v = y;
+      if (which < 2 && ri.is_img) {
+        const int gw = meta.grid_w[ri.req];
+        const int half = d >> 1;
+        const int pos = (dd < half) ? (ri.local / gw) : (ri.local % gw);
+        const int kk = (dd < half ? dd : dd - half) >> 1;
+        const float2 cs = e.rope[pos * (d >> 2) + kk];
+        // even: u cos - v sin ; odd: u sin + v cos  (u = even element, v = odd element)
+        v = (dd & 1) ? (y_pair * cs.y + y * cs.x) : (y * cs.x - y_pair * cs.y);
+      }
+      if (which == 0)
+        ((T*)e.q)[((long)h * e.T + p) * d + dd] = from_f32<T>(v);
+      else if (which == 1)
+        ((T*)e.k)[((long)h * e.T + p) * d + dd] = from_f32<T>(v);
+      else
+        ((T*)e.vt)[((long)h * d + dd) * e.T + p] = from_f32<T>(v);
+      break;
+    }
+    default:
+      break;
+  }
+}
+
+// XCD-aware block remap: hardware dispatches block b to XCD b % 8; return an
+// index such that every XCD owns one contiguous range of indices.
+__device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
+  const int per = nblocks / 8, rem = nblocks % 8;
+  const int xcd = bid % 8, idx = bid / 8;
+  return (xcd < rem) ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
+}
+
+}  // namespace dit

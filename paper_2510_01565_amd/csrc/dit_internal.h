@@ -1,0 +1,172 @@
+// Internal structures shared by the host orchestration and the HIP kernels.
+// Everything a kernel needs about a packed batch travels by value in its
+// arguments (BatchMeta), so no metadata is ever uploaded to the device.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/dit.h"
+
+namespace dit {
+
+constexpr int kMaxReq = DIT_MAX_REQUESTS;
+
+// Row bookkeeping of a packed batch.
+//  stream-major rows: [text of req 0 .. text of req n-1 | image of req 0 .. image of req n-1]
+//  joint positions:   [req 0: text, image | req 1: text, image | ...]  (attention order)
+struct BatchMeta {
+  int n_req;
+  int T_txt;                 // total text rows
+  int T_img;                 // total image rows
+  int T;                     // T_txt + T_img
+  int txt_off[kMaxReq + 1];  // text row offsets (stream-major)
+  int img_off[kMaxReq + 1];  // image row offsets, relative to T_txt
+  int joint_off[kMaxReq + 1];
+  int pad_off[kMaxReq + 1];  // joint offsets with every request padded to a multiple of 64
+  int n_txt[kMaxReq];
+  int grid_w[kMaxReq];
+};
+
+constexpr int kSeqPad = 64;
+
+struct RowInfo {
+  int req;     // request index
+  int is_img;  // 1 for image tokens
+  int local;   // index inside the request's text or image rows
+};
+
+__host__ __device__ inline RowInfo row_info(const BatchMeta& m, int R) {
+  RowInfo ri;
+  if (R < m.T_txt) {
+    int r = 0;
+    while (r + 1 < m.n_req && R >= m.txt_off[r + 1]) ++r;
+    ri.req = r;
+    ri.is_img = 0;
+    ri.local = R - m.txt_off[r];
+  } else {
+    int Ri = R - m.T_txt;
+    int r = 0;
+    while (r + 1 < m.n_req && Ri >= m.img_off[r + 1]) ++r;
+    ri.req = r;
+    ri.is_img = 1;
+    ri.local = Ri - m.img_off[r];
+  }
+  return ri;
+}
+
+// position of a row inside the padded joint layout of Q, K and V^T
+__host__ __device__ inline int padded_pos(const BatchMeta& m, const RowInfo& ri) {
+  return m.pad_off[ri.req] + (ri.is_img ? m.n_txt[ri.req] : 0) + ri.local;
+}
+
+// joint position -> stream-major row
+__host__ __device__ inline int joint_to_row(const BatchMeta& m, int p) {
+  int r = 0;
+  while (r + 1 < m.n_req && p >= m.joint_off[r + 1]) ++r;
+  int loc = p - m.joint_off[r];
+  if (loc < m.n_txt[r]) return m.txt_off[r] + loc;
+  return m.T_txt + m.img_off[r] + (loc - m.n_txt[r]);
+}
+
+// ----------------------------------------------------------------------------
+// GEMM epilogues: Y = A W^T + bias, then one of
+enum EpiMode : int {
+  EPI_STORE_F32 = 0,  // out[m, n] = y (fp32)
+  EPI_STORE_T = 1,    // out[m, n] = y (storage type: bf16 or fp32)
+  EPI_GELU = 2,       // out[m, col0 + n] = GELU(y)
+  EPI_RESID = 3,      // out[m, n] (fp32) += gate[req(m), n] * y
+  EPI_QKV = 4         // n < n_qkv: Q/K/V scatter with 2-D RoPE on image rows;
+                      // n >= n_qkv: gelu_out[m, gelu_col0 + n - n_qkv] = GELU(y)
+};
+
+struct EpiArgs {
+  int mode;
+  int row_base;         // stream-major row of the group's row 0 (request lookup)
+  const void* bias;     // [N], weight type, may be null
+  void* out;            // already offset to the group's row 0
+  long ldo;
+  int col0;
+  const float* mods;    // EPI_RESID: gate = mods[req * mods_ld + gate_off + n]
+  int mods_ld;
+  int gate_off;
+  // EPI_QKV
+  void* q;              // [heads][T][d]
+  void* k;              // [heads][T][d]
+  void* vt;             // [heads][d][T]
+  int T;                // padded joint length (pad_off[n_req])
+  int hidden;
+  int head_dim;
+  int n_qkv;            // 3 * hidden
+  const float2* rope;   // [DIT_MAX_GRID][head_dim / 4] (cos, sin)
+  void* gelu_out;
+  long gelu_ld;
+  int gelu_col0;
+};
+
+struct GemmGroup {
+  const void* A;  // [M, K], lda
+  long lda;
+  const void* W;  // [N, K], ldw
+  long ldw;
+  int M;
+  int K;
+  EpiArgs epi;
+};
+
+struct GemmProblem {
+  int N;
+  int n_groups;  // 1 or 2
+  GemmGroup g[2];
+  BatchMeta meta;
+};
+
+// ----------------------------------------------------------------------------
+// launchers (return hipError_t of the launch)
+hipError_t launch_gemm_bf16(const GemmProblem& p, hipStream_t s);
+hipError_t launch_gemm_f32(const GemmProblem& p, hipStream_t s);
+// name of the kernel configuration launch_gemm_bf16 picks for p
+const char* gemm_bf16_config_name(const GemmProblem& p);
+
+// Attention over the requests of a batch.  Token p of request r (joint
+// order, 0 <= p < L_r) is read from Q/K row qk_off[r] + p and from V^T
+// column vt_off[r] + p; V^T columns of a request are padded to a multiple of
+// 64 (vt_off from pad_off) so that a 64-key tile never leaves the buffer.
+struct AttnArgs {
+  const void* q;
+  long q_tok, q_head;   // element strides
+  const void* k;
+  long k_tok, k_head;
+  const void* vt;       // Vt[h][dd][vt column]
+  long vt_head, vt_d;
+  void* o;
+  long o_tok, o_head;
+  int o_stream_major;   // 1: output row = joint_to_row(joint_off[r] + p); 0: joint_off[r] + p
+  int heads;
+  int head_dim;
+  float scale;          // 1/sqrt(head_dim)
+  int qk_off[kMaxReq + 1];
+  int vt_off[kMaxReq + 1];
+  BatchMeta meta;
+};
+hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s);
+hipError_t launch_attention_f32(const AttnArgs& a, hipStream_t s);
+
+// elementwise / reduction kernels
+hipError_t launch_rope_table(float2* table, int head_dim, float theta, hipStream_t s);
+hipError_t launch_timestep_embed(float* e, int n_req, const float* t_host, int dim, hipStream_t s);
+// y[r, o] = sum_k W[o, k] * act(x[r, k]) + b[o]; act 0 = identity, 1 = SiLU
+hipError_t launch_gemv(int wdtype, const void* W, const void* b, const float* x, long ldx, int n_req,
+                       int K, int N, int act, float* y, long ldy, hipStream_t s);
+// adaLN LayerNorm of rows [row_begin, row_end) of X (fp32, ld H) into out (row 0 = row_begin)
+hipError_t launch_ln_modulate(int out_dtype, const float* X, int H, int row_begin, int row_end,
+                              const BatchMeta& meta, const float* mods, int mods_ld, int shift_txt,
+                              int scale_txt, int shift_img, int scale_img, float eps, void* out,
+                              long ldo, hipStream_t s);
+hipError_t launch_euler(int dtype, void* x, const void* v, int channels, const BatchMeta& meta,
+                        const float* dt_host, hipStream_t s);
+// v [T_joint, heads, d] (joint order) -> vt [heads][d][pad_off[n]] at padded columns
+hipError_t launch_v_transpose(int dtype, const void* v, const BatchMeta& meta, int heads, int d, void* vt,
+                              hipStream_t s);
+
+}  // namespace dit

@@ -1,0 +1,291 @@
+// HBM-bound kernels of the step: adaLN LayerNorm, the modulation GEMV over
+// all blocks' adaLN weights, the timestep embedding, the RoPE angle table,
+// the Euler update and the V relayout of the stand-alone attention call.
+// Rows are processed one per wavefront with 16-byte accesses; all reductions
+// are fixed butterfly trees (bitwise deterministic).
+#include <math.h>
+
+#include "device_common.h"
+
+namespace dit {
+
+namespace {
+
+// ---------------------------------------------------------------- RoPE table
+// table[pos][k] = (cos, sin)(pos * theta^(-2k / (d/2))), evaluated in fp64.
+__global__ void rope_table_kernel(float2* table, int quarter, int axis_dim, double theta) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= DIT_MAX_GRID * quarter) return;
+  const int pos = i / quarter, k = i % quarter;
+  const double ang = (double)pos * pow(theta, -2.0 * k / axis_dim);
+  table[i] = make_float2((float)cos(ang), (float)sin(ang));
+}
+
+// ---------------------------------------------------------------- timestep embedding
+// e[r] = [cos(1000 t f_j) | sin(1000 t f_j)], f_j = 1e4^(-j/half), in fp64.
+struct TimeArgs {
+  float t[kMaxReq];
+};
+__global__ void timestep_kernel(float* e, int n_req, TimeArgs ta, int dim) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  const int half = dim / 2;
+  if (i >= n_req * half) return;
+  const int r = i / half, j = i % half;
+  const double f = exp(-log(10000.0) * (double)j / half);
+  const double ang = 1000.0 * (double)ta.t[r] * f;
+  e[(long)r * dim + j] = (float)cos(ang);
+  e[(long)r * dim + half + j] = (float)sin(ang);
+}
+
+// ---------------------------------------------------------------- GEMV
+// y[r, o] = sum_k W[o, k] act(x[r, k]) + b[o] for up to 4 requests per pass;
+// one wavefront per output row, activations staged in LDS, weights streamed
+// once with 16-byte loads.
+constexpr int GV_R = 4;
+
+template <typename WT>
+__global__ __launch_bounds__(256) void gemv_kernel(const WT* __restrict__ W, const WT* __restrict__ b,
+                                                   const float* __restrict__ x, long ldx, int n_req, int K,
+                                                   int N, int act, float* __restrict__ y, long ldy) {
+  extern __shared__ float xs[];  // [GV_R][K]
+  const int nr = min(n_req, GV_R);
+  for (int i = threadIdx.x; i < nr * K; i += blockDim.x) {
+    const int r = i / K, k = i % K;
+    float v = x[(long)r * ldx + k];
+    xs[i] = act ? silu(v) : v;
+  }
+  __syncthreads();
+  constexpr int EPC = 16 / sizeof(WT);  // elements per 16-byte chunk
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int nwaves = (gridDim.x * blockDim.x) >> 6;
+  const int chunks = K / EPC;
+  for (int o = blockIdx.x * 4 + wave; o < N; o += nwaves) {
+    float acc[GV_R] = {0.f, 0.f, 0.f, 0.f};
+    const WT* wr = W + (long)o * K;
+    for (int c = lane; c < chunks; c += 64) {
+      const uint4 u = *(const uint4*)(wr + c * EPC);
+      float wv[EPC];
+      if constexpr (sizeof(WT) == 2) {
+        const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          wv[2 * e] = __uint_as_float(w4[e] << 16);
+          wv[2 * e + 1] = __uint_as_float(w4[e] & 0xFFFF0000u);
+        }
+      } else {
+        wv[0] = __uint_as_float(u.x);
+        wv[1] = __uint_as_float(u.y);
+        wv[2] = __uint_as_float(u.z);
+        wv[3] = __uint_as_float(u.w);
+      }
+#pragma unroll
+      for (int r = 0; r < GV_R; ++r) {
+        if (r < nr) {
+          const float* xr = xs + r * K + c * EPC;
+#pragma unroll
+          for (int e = 0; e < EPC; ++e) acc[r] = fmaf(wv[e], xr[e], acc[r]);
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < GV_R; ++r) {
+      if (r < nr) {
+        const float s = wave_sum(acc[r]);
+        if (lane == 0) y[(long)r * ldy + o] = s + (b ? to_f32<WT>(b[o]) : 0.f);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- adaLN LayerNorm
+// out = LN(x) * (1 + scale[req]) + shift[req], LN with biased variance and no
+// affine; statistics in fp32 with a two-pass (mean, then centred squares)
+// evaluation from registers.  One wavefront per row; H <= 64 * 4 * 16.
+constexpr int LN_MAXV = 16;  // float4 per lane
+
+template <typename OT>
+__global__ __launch_bounds__(256) void ln_mod_kernel(const float* __restrict__ X, int H, int row_begin,
+                                                     int row_end, const BatchMeta meta,
+                                                     const float* __restrict__ mods, int mods_ld, int sh_t,
+                                                     int sc_t, int sh_i, int sc_i, float eps, OT* __restrict__ out,
+                                                     long ldo) {
+  const int lane = threadIdx.x & 63;
+  const int R = row_begin + blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (R >= row_end) return;
+  const int H4 = H >> 2;
+  const float4* xr = (const float4*)(X + (long)R * H);
+  float4 v[LN_MAXV];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < LN_MAXV; ++i) {
+    const int c = lane + i * 64;
+    if (c < H4) {
+      v[i] = xr[c];
+      s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
+    }
+  }
+  const float mean = wave_sum(s) / (float)H;
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < LN_MAXV; ++i) {
+    const int c = lane + i * 64;
+    if (c < H4) {
+      v[i].x -= mean;
+      v[i].y -= mean;
+      v[i].z -= mean;
+      v[i].w -= mean;
+      ss += (v[i].x * v[i].x + v[i].y * v[i].y) + (v[i].z * v[i].z + v[i].w * v[i].w);
+    }
+  }
+  const float rstd = 1.0f / sqrtf(wave_sum(ss) / (float)H + eps);
+  const RowInfo ri = row_info(meta, R);
+  const float* mrow = mods + (long)ri.req * mods_ld;
+  const float4* shv = (const float4*)(mrow + (ri.is_img ? sh_i : sh_t));
+  const float4* scv = (const float4*)(mrow + (ri.is_img ? sc_i : sc_t));
+  OT* orow = out + (long)(R - row_begin) * ldo;
+#pragma unroll
+  for (int i = 0; i < LN_MAXV; ++i) {
+    const int c = lane + i * 64;
+    if (c < H4) {
+      const float4 sh = shv[c], sc = scv[c];
+      const float y0 = v[i].x * rstd * (1.f + sc.x) + sh.x;
+      const float y1 = v[i].y * rstd * (1.f + sc.y) + sh.y;
+      const float y2 = v[i].z * rstd * (1.f + sc.z) + sh.z;
+      const float y3 = v[i].w * rstd * (1.f + sc.w) + sh.w;
+      if constexpr (sizeof(OT) == 2) {
+        uint2 w;
+        w.x = pack_bf16x2(y0, y1);
+        w.y = pack_bf16x2(y2, y3);
+        *(uint2*)(orow + c * 4) = w;
+      } else {
+        *(float4*)(orow + c * 4) = make_float4(y0, y1, y2, y3);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- Euler
+struct DtArgs {
+  float dt[kMaxReq];
+};
+template <typename T>
+__global__ void euler_kernel(T* __restrict__ x, const T* __restrict__ v, long n, int channels, const BatchMeta meta,
+                             DtArgs da) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int row = (int)(i / channels);
+  int r = 0;
+  while (r + 1 < meta.n_req && row >= meta.img_off[r + 1]) ++r;
+  const float xv = to_f32<T>(x[i]), vv = to_f32<T>(v[i]);
+  x[i] = from_f32<T>(xv - da.dt[r] * vv);
+}
+
+// ---------------------------------------------------------------- V relayout
+template <typename T>
+__global__ void v_transpose_kernel(const T* __restrict__ v, const BatchMeta meta, int heads, int d,
+                                   T* __restrict__ vt, long ld) {
+  __shared__ T tile[32][33];
+  const int h = blockIdx.z;
+  const int p0 = blockIdx.x * 32, d0 = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
+  const int T_ = meta.T;
+  for (int yy = ty; yy < 32; yy += 8) {
+    const int p = p0 + yy, dd = d0 + tx;
+    if (p < T_ && dd < d) tile[yy][tx] = v[((long)p * heads + h) * d + dd];
+  }
+  __syncthreads();
+  for (int yy = ty; yy < 32; yy += 8) {
+    const int dd = d0 + yy, p = p0 + tx;
+    if (p < T_ && dd < d) {
+      int r = 0;
+      while (r + 1 < meta.n_req && p >= meta.joint_off[r + 1]) ++r;
+      const int col = meta.pad_off[r] + (p - meta.joint_off[r]);
+      vt[((long)h * d + dd) * ld + col] = tile[tx][yy];
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_rope_table(float2* table, int head_dim, float theta, hipStream_t s) {
+  const int quarter = head_dim / 4;
+  const int n = DIT_MAX_GRID * quarter;
+  hipLaunchKernelGGL(rope_table_kernel, dim3((n + 255) / 256), dim3(256), 0, s, table, quarter, head_dim / 2,
+                     (double)theta);
+  return hipGetLastError();
+}
+
+hipError_t launch_timestep_embed(float* e, int n_req, const float* t_host, int dim, hipStream_t s) {
+  TimeArgs ta{};
+  for (int r = 0; r < n_req; ++r) ta.t[r] = t_host[r];
+  const int n = n_req * (dim / 2);
+  hipLaunchKernelGGL(timestep_kernel, dim3((n + 255) / 256), dim3(256), 0, s, e, n_req, ta, dim);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemv(int wdtype, const void* W, const void* b, const float* x, long ldx, int n_req, int K,
+                       int N, int act, float* y, long ldy, hipStream_t s) {
+  const size_t shmem = (size_t)GV_R * K * sizeof(float);
+  int blocks = (N + 3) / 4;
+  if (blocks > 256 * 16) blocks = 256 * 16;
+  for (int r0 = 0; r0 < n_req; r0 += GV_R) {
+    const int nr = n_req - r0 < GV_R ? n_req - r0 : GV_R;
+    if (wdtype == DIT_BF16)
+      hipLaunchKernelGGL(gemv_kernel<bf16_t>, dim3(blocks), dim3(256), shmem, s, (const bf16_t*)W,
+                         (const bf16_t*)b, x + (long)r0 * ldx, ldx, nr, K, N, act, y + (long)r0 * ldy, ldy);
+    else
+      hipLaunchKernelGGL(gemv_kernel<float>, dim3(blocks), dim3(256), shmem, s, (const float*)W, (const float*)b,
+                         x + (long)r0 * ldx, ldx, nr, K, N, act, y + (long)r0 * ldy, ldy);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_ln_modulate(int out_dtype, const float* X, int H, int row_begin, int row_end,
+                              const BatchMeta& meta, const float* mods, int mods_ld, int shift_txt, int scale_txt,
+                              int shift_img, int scale_img, float eps, void* out, long ldo, hipStream_t s) {
+  const int rows = row_end - row_begin;
+  if (rows <= 0) return hipSuccess;
+  const dim3 grid((rows + 3) / 4);
+  if (out_dtype == DIT_BF16)
+    hipLaunchKernelGGL(ln_mod_kernel<bf16_t>, grid, dim3(256), 0, s, X, H, row_begin, row_end, meta, mods, mods_ld,
+                       shift_txt, scale_txt, shift_img, scale_img, eps, (bf16_t*)out, ldo);
+  else
+    hipLaunchKernelGGL(ln_mod_kernel<float>, grid, dim3(256), 0, s, X, H, row_begin, row_end, meta, mods, mods_ld,
+                       shift_txt, scale_txt, shift_img, scale_img, eps, (float*)out, ldo);
+  return hipGetLastError();
+}
+
+hipError_t launch_euler(int dtype, void* x, const void* v, int channels, const BatchMeta& meta,
+                        const float* dt_host, hipStream_t s) {
+  DtArgs da{};
+  for (int r = 0; r < meta.n_req; ++r) da.dt[r] = dt_host[r];
+  const long n = (long)meta.T_img * channels;
+  if (n == 0) return hipSuccess;
+  const dim3 grid((unsigned)((n + 255) / 256));
+  if (dtype == DIT_BF16)
+    hipLaunchKernelGGL(euler_kernel<bf16_t>, grid, dim3(256), 0, s, (bf16_t*)x, (const bf16_t*)v, n, channels, meta,
+                       da);
+  else
+    hipLaunchKernelGGL(euler_kernel<float>, grid, dim3(256), 0, s, (float*)x, (const float*)v, n, channels, meta,
+                       da);
+  return hipGetLastError();
+}
+
+hipError_t launch_v_transpose(int dtype, const void* v, const BatchMeta& meta, int heads, int d, void* vt,
+                              hipStream_t s) {
+  const long ld = meta.pad_off[meta.n_req];
+  const dim3 grid((meta.T + 31) / 32, (d + 31) / 32, heads);
+  if (meta.T == 0) return hipSuccess;
+  if (dtype == DIT_BF16)
+    hipLaunchKernelGGL(v_transpose_kernel<bf16_t>, grid, dim3(256), 0, s, (const bf16_t*)v, meta, heads, d,
+                       (bf16_t*)vt, ld);
+  else
+    hipLaunchKernelGGL(v_transpose_kernel<float>, grid, dim3(256), 0, s, (const float*)v, meta, heads, d, (float*)vt,
+                       ld);
+  return hipGetLastError();
+}
+
+}  // namespace dit

@@ -1,0 +1,136 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every function that include/dit.h declares, describes the same parameter set
+as the oracle, sizes workspaces, and rejects invalid calls before enqueuing
+anything."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle as O
+from paper_2510_01565_amd import dit, workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _header_functions():
+    src = open(os.path.join(ROOT, "include", "dit.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:dit_status|const char\*)\s+(\w+)\s*\(", src, flags=re.M)))
+
+
+def test_library_exports_every_header_function():
+    names = _header_functions()
+    assert len(names) >= 10
+    L = dit.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(dit.EXPORTED)
+
+
+def _oracle_cfg(m: workloads.ModelShape):
+    return O.OracleConfig(hidden=m.hidden, heads=m.heads, head_dim=m.head_dim, mlp_ratio=m.mlp_ratio,
+                          n_double=m.n_double, n_single=m.n_single, in_channels=m.in_channels,
+                          text_dim=m.text_dim, time_freq_dim=m.time_freq_dim, tie_streams=m.tie_streams)
+
+
+@pytest.mark.parametrize("name", ["small_block_256px_f32", "mmdit_double_512px_bf16", "dit57_1024px_bf16"])
+def test_manifest_matches_oracle_parameter_set(name):
+    m = workloads.WORKLOADS[name].model
+    got = dit.weight_manifest(dit.make_config(m))
+    assert got == [(n, tuple(s)) for n, s in O.param_shapes(_oracle_cfg(m))]
+
+
+def test_full_model_parameter_count():
+    m = workloads.FLUX_FULL
+    n = sum(int(__import__("numpy").prod(s)) for _, s in dit.weight_manifest(dit.make_config(m)))
+    # 19 double + 38 single blocks at 3072 wide: ~11.9e9 parameters, 3.25e9 of them adaLN modulation
+    assert 11.8e9 < n < 12.0e9
+    mod = [s for nm, s in dit.weight_manifest(dit.make_config(m)) if nm == "mod.w"][0]
+    assert mod == ((19 * 12 + 38 * 3 + 2) * 3072, 3072)
+
+
+def test_workspace_size_grows_with_tokens():
+    cfg = dit.make_config(workloads.FLUX_FULL)
+    a = dit.workspace_size(cfg, dit.Batch([64], [64], [512], [0.5]))
+    b = dit.workspace_size(cfg, dit.Batch([128], [128], [512], [0.5]))
+    c = dit.workspace_size(cfg, dit.Batch([16, 32, 64, 128], [16, 32, 64, 128], [512] * 4, [0.1, 0.2, 0.3, 0.4]))
+    assert 0 < a < b < c
+    assert c < 4 * 2 ** 30     # the 23808-token packed step needs only a few GB of scratch
+
+
+def _err(fn, *args):
+    with pytest.raises(dit.DitError) as e:
+        fn(*args)
+    return e.value.status
+
+
+def test_invalid_configs_are_rejected():
+    base = workloads.FLUX_FULL
+    cfg = dit.make_config(base)
+    cfg.heads = 23
+    assert _err(dit.weight_count, cfg) == dit.DIT_ERR_INVALID_ARG
+    cfg = dit.make_config(base)
+    cfg.head_dim, cfg.heads = 64, 48
+    assert _err(dit.weight_count, cfg) == dit.DIT_ERR_UNSUPPORTED
+    cfg = dit.make_config(base)
+    cfg.in_channels = 12
+    assert _err(dit.weight_count, cfg) == dit.DIT_ERR_UNSUPPORTED
+    cfg = dit.make_config(base)
+    cfg.dtype = 7
+    assert _err(dit.weight_count, cfg) == dit.DIT_ERR_INVALID_ARG
+    assert "dtype" in dit.lib().dit_last_error().decode()
+
+
+def test_invalid_batches_are_rejected():
+    cfg = dit.make_config(workloads.FLUX_FULL)
+    assert _err(dit.workspace_size, cfg, dit.Batch([], [], [])) == dit.DIT_ERR_INVALID_ARG
+    assert _err(dit.workspace_size, cfg, dit.Batch([1] * 17, [1] * 17, [0] * 17)) == dit.DIT_ERR_INVALID_ARG
+    assert _err(dit.workspace_size, cfg, dit.Batch([0], [4], [1])) == dit.DIT_ERR_INVALID_ARG
+    assert _err(dit.workspace_size, cfg, dit.Batch([257], [4], [1])) == dit.DIT_ERR_INVALID_ARG
+    assert _err(dit.workspace_size, cfg, dit.Batch([4], [4], [-1])) == dit.DIT_ERR_INVALID_ARG
+
+
+def test_dit_step_validation_happens_before_any_launch():
+    """Every one of these calls fails on the host; none reaches the GPU."""
+    m = workloads.SMALL_BLOCK
+    cfg = dit.make_config(m)
+    n = dit.weight_count(cfg)
+    fake = dit.Weights([4096 * (i + 1) for i in range(n)])
+    b = dit.Batch([16], [16], [32], [0.5])
+    need = dit.workspace_size(cfg, b)
+    P = 1 << 20
+    # missing timesteps
+    assert _err(dit.dit_step, cfg, fake, dit.Batch([16], [16], [32]), P, P, P, P, need, 0) == dit.DIT_ERR_INVALID_ARG
+    # timestep outside [0, 1]
+    assert _err(dit.dit_step, cfg, fake, dit.Batch([16], [16], [32], [1.5]), P, P, P, P, need, 0) == \
+        dit.DIT_ERR_INVALID_ARG
+    # wrong number of weights
+    assert _err(dit.dit_step, cfg, dit.Weights([4096] * (n - 1)), b, P, P, P, P, need, 0) == dit.DIT_ERR_INVALID_ARG
+    # misaligned weight
+    bad = dit.Weights([4096 * (i + 1) + (8 if i == 3 else 0) for i in range(n)])
+    assert _err(dit.dit_step, cfg, bad, b, P, P, P, P, need, 0) == dit.DIT_ERR_INVALID_ARG
+    # null latents
+    assert _err(dit.dit_step, cfg, fake, b, 0, P, P, P, need, 0) == dit.DIT_ERR_INVALID_ARG
+    # workspace too small / null / misaligned
+    assert _err(dit.dit_step, cfg, fake, b, P, P, P, P, need - 1, 0) == dit.DIT_ERR_WORKSPACE
+    assert _err(dit.dit_step, cfg, fake, b, P, P, P, 0, need, 0) == dit.DIT_ERR_WORKSPACE
+    assert _err(dit.dit_step, cfg, fake, b, P, P, P, P + 64, need, 0) == dit.DIT_ERR_WORKSPACE
+    # block index out of range, bad kind
+    assert _err(dit.dit_block_forward, cfg, fake, 0, 1, b, P, P, P, need, 0) == dit.DIT_ERR_INVALID_ARG
+    assert _err(dit.dit_block_forward, cfg, fake, 2, 0, b, P, P, P, need, 0) == dit.DIT_ERR_INVALID_ARG
+    # attention head_dim unsupported for the dtype
+    assert _err(dit.dit_attention, b, 6, 64, dit.DIT_BF16, P, P, P, P, P, need, 0) == dit.DIT_ERR_UNSUPPORTED
+    # GEMM K not a multiple of 8
+    assert _err(dit.dit_linear, 4, 4, 12, dit.DIT_BF16, P, P, 0, P, dit.DIT_F32, 0) == dit.DIT_ERR_UNSUPPORTED
+    # Euler with a non-finite dt
+    assert _err(dit.euler_update, b, 16, dit.DIT_F32, P, P, [float("nan")], 0) == dit.DIT_ERR_INVALID_ARG
+
+
+def test_last_error_is_cleared_by_a_good_call():
+    cfg = dit.make_config(workloads.FLUX_FULL)
+    _err(dit.workspace_size, cfg, dit.Batch([0], [4], [1]))
+    assert dit.lib().dit_last_error().decode() != ""
+    dit.weight_count(cfg)
+    assert dit.lib().dit_last_error().decode() == ""

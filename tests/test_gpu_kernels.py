@@ -1,0 +1,131 @@
+"""Kernel-level parity on the GPU: each entry point of the C ABI against the
+oracle on the same seeded inputs, at sizes that span several tiles and end
+in ragged tails."""
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2510_01565_amd import dit, synth
+from harness import BF16_TOL, F32_TOL, normwise_err, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    return torch
+
+
+@pytest.mark.parametrize("M,N,K", [(77, 64, 40), (300, 200, 136), (2500, 1100, 520), (513, 3072, 3072)])
+@pytest.mark.parametrize("out", ["f32", "bf16"])
+def test_linear_bf16(M, N, K, out):
+    torch = _torch()
+    x = synth.normal(1, "x", (M, K), bf16=True)
+    w = synth.normal(1, "w", (N, K), std=0.02, bf16=True)
+    b = synth.normal(1, "b", (N,), std=0.02, bf16=True)
+    ref = O.linear(x.astype(np.float64), w.astype(np.float64), b.astype(np.float64))
+    od = torch.float32 if out == "f32" else torch.bfloat16
+    y = torch.empty((M, N), dtype=od, device="cuda")
+    dit.dit_linear(M, N, K, dit.DIT_BF16, to_dev(x, torch.bfloat16), to_dev(w, torch.bfloat16),
+                   to_dev(b, torch.bfloat16), y, dit.DIT_F32 if out == "f32" else dit.DIT_BF16)
+    torch.cuda.synchronize()
+    err = normwise_err(y.float().cpu().numpy(), ref)
+    assert err < (F32_TOL if out == "f32" else BF16_TOL), err
+    if out == "bf16":
+        # every element within 2 bf16 ulps of the exact value
+        g = y.float().cpu().numpy()
+        assert np.all(np.abs(g - ref) <= 2 ** -7 * np.abs(ref) + 1e-6 * np.abs(ref).max())
+
+
+@pytest.mark.parametrize("M,N,K", [(5, 3, 8), (130, 70, 200), (300, 1152, 384)])
+def test_linear_f32(M, N, K):
+    torch = _torch()
+    x = synth.normal(2, "x", (M, K))
+    w = synth.normal(2, "w", (N, K), std=0.02)
+    b = synth.normal(2, "b", (N,), std=0.02)
+    ref = O.linear(x.astype(np.float64), w.astype(np.float64), b.astype(np.float64))
+    y = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    dit.dit_linear(M, N, K, dit.DIT_F32, to_dev(x, torch.float32), to_dev(w, torch.float32),
+                   to_dev(b, torch.float32), y, dit.DIT_F32)
+    torch.cuda.synchronize()
+    assert normwise_err(y.cpu().numpy(), ref) < F32_TOL
+
+
+def _attn_case(grids, n_txt, heads, d, bf16, seed):
+    torch = _torch()
+    lens = [gh * gw + nt for (gh, gw), nt in zip(grids, n_txt)]
+    T = sum(lens)
+    q = synth.normal(seed, "q", (T, heads, d), bf16=bf16)
+    k = synth.normal(seed, "k", (T, heads, d), bf16=bf16)
+    v = synth.normal(seed, "v", (T, heads, d), bf16=bf16)
+    ref = np.empty((T, heads, d))
+    off = 0
+    for L in lens:
+        sl = slice(off, off + L)
+        ref[sl] = O.attention(q[sl].astype(np.float64), k[sl].astype(np.float64), v[sl].astype(np.float64))
+        off += L
+    dt = torch.bfloat16 if bf16 else torch.float32
+    b = dit.Batch([g[0] for g in grids], [g[1] for g in grids], n_txt)
+    dtype = dit.DIT_BF16 if bf16 else dit.DIT_F32
+    wsb = dit.attention_workspace_size(b, heads, d, dtype)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    o = torch.full((T, heads, d), float("nan"), dtype=dt, device="cuda")
+    dit.dit_attention(b, heads, d, dtype, to_dev(q, dt), to_dev(k, dt), to_dev(v, dt), o, ws, wsb)
+    torch.cuda.synchronize()
+    return o.float().cpu().numpy(), ref
+
+
+@pytest.mark.parametrize("grids,n_txt", [
+    ([(16, 16)], [32]),                       # 288 tokens: 2 full + 1 partial query tile, ragged key tile
+    ([(5, 7), (16, 16), (9, 13)], [3, 32, 17]),  # packed, lengths 38 / 288 / 134
+    ([(1, 1)], [0]),                          # a single token
+])
+def test_attention_bf16(grids, n_txt):
+    got, ref = _attn_case(grids, n_txt, 3, 128, True, 3)
+    assert normwise_err(got, ref) < BF16_TOL
+
+
+@pytest.mark.parametrize("grids,n_txt", [([(16, 16)], [32]), ([(5, 7), (9, 13)], [3, 17])])
+def test_attention_f32(grids, n_txt):
+    got, ref = _attn_case(grids, n_txt, 2, 64, False, 4)
+    assert normwise_err(got, ref) < F32_TOL
+
+
+def test_attention_identical_keys_give_mean_of_values():
+    torch = _torch()
+    T, heads, d = 200, 2, 128
+    q = synth.normal(5, "q", (T, heads, d), bf16=True)
+    k = np.broadcast_to(synth.normal(5, "k", (1, heads, d), bf16=True), (T, heads, d)).copy()
+    v = synth.normal(5, "v", (T, heads, d), bf16=True)
+    b = dit.Batch([10], [18], [20])
+    wsb = dit.attention_workspace_size(b, heads, d, dit.DIT_BF16)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    o = torch.empty((T, heads, d), dtype=torch.bfloat16, device="cuda")
+    dit.dit_attention(b, heads, d, dit.DIT_BF16, to_dev(q, torch.bfloat16), to_dev(k, torch.bfloat16),
+                      to_dev(v, torch.bfloat16), o, ws, wsb)
+    torch.cuda.synchronize()
+    ref = np.broadcast_to(v.astype(np.float64).mean(0), v.shape)
+    assert normwise_err(o.float().cpu().numpy(), ref) < BF16_TOL
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_euler(bf16):
+    torch = _torch()
+    grids = [(3, 5), (8, 8)]
+    C = 16
+    n = sum(g[0] * g[1] for g in grids)
+    x = synth.normal(6, "x", (n, C), bf16=bf16)
+    v = synth.normal(6, "v", (n, C), bf16=bf16)
+    dts = [1 / 28, 0.3]
+    dt = torch.bfloat16 if bf16 else torch.float32
+    xd = to_dev(x, dt)
+    b = dit.Batch([g[0] for g in grids], [g[1] for g in grids], [0, 0])
+    dit.euler_update(b, C, dit.DIT_BF16 if bf16 else dit.DIT_F32, xd, to_dev(v, dt), dts)
+    torch.cuda.synchronize()
+    ref = np.concatenate([O.euler_update(x[:15].astype(np.float64), v[:15].astype(np.float64), dts[0]),
+                          O.euler_update(x[15:].astype(np.float64), v[15:].astype(np.float64), dts[1])])
+    got = xd.float().cpu().numpy()
+    if bf16:
+        assert np.all(np.abs(got - ref) <= 2 ** -8 * np.abs(ref) + 1e-30)
+    else:
+        assert np.all(np.abs(got - ref) <= 1e-6 * np.abs(ref) + 1e-7)
