@@ -5,9 +5,24 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+#include <utility>
+
 #include "dit_internal.h"
 
 namespace dit {
+
+// Compile-time loop: f(std::integral_constant<int, 0>) ... f(<N-1>).  Register
+// arrays indexed by its counter never become dynamically indexed (which would
+// move them to scratch memory).
+template <class F, int... Is>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
+  (f(std::integral_constant<int, Is>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
 
 typedef uint16_t bf16_t;  // raw bfloat16 storage
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -49,11 +64,35 @@ __device__ __forceinline__ float gelu_tanh(float x) {
 
 __device__ __forceinline__ float silu(float x) { return x / (1.0f + __expf(-x)); }
 
+// Per-row facts an epilogue needs, computed once per output tile row.
+struct RowEntry {
+  int req;  // request index
+  int pos;  // position in the padded joint layout of Q / K / V^T
+  int gi;   // grid row of an image token, -1 for text
+  int gj;   // grid column of an image token
+};
+
+__device__ __forceinline__ RowEntry make_row_entry(const BatchMeta& meta, int R) {
+  const RowInfo ri = row_info(meta, R);
+  RowEntry e;
+  e.req = ri.req;
+  e.pos = padded_pos(meta, ri);
+  if (ri.is_img) {
+    const int gw = meta.grid_w[ri.req];
+    e.gi = ri.local / gw;
+    e.gj = ri.local - e.gi * gw;
+  } else {
+    e.gi = -1;
+    e.gj = 0;
+  }
+  return e;
+}
+
 // One output element of a GEMM epilogue.  `y` already includes the bias;
 // `y_pair` is the value of the partner column n ^ 1 (RoPE pairs), bias included.
 template <typename T>
-__device__ __forceinline__ void epilogue_element(const EpiArgs& e, const BatchMeta& meta, int m, int n,
-                                                 float y, float y_pair) {
+__device__ __forceinline__ void epilogue_element(const EpiArgs& e, const RowEntry& row, int m, int n, float y,
+                                                 float y_pair) {
   switch (e.mode) {
     case EPI_STORE_F32:
       ((float*)e.out)[(long)m * e.ldo + n] = y;
@@ -65,8 +104,7 @@ __device__ __forceinline__ void epilogue_element(const EpiArgs& e, const BatchMe
       ((T*)e.out)[(long)m * e.ldo + e.col0 + n] = from_f32<T>(gelu_tanh(y));
       break;
     case EPI_RESID: {
-      RowInfo ri = row_info(meta, e.row_base + m);
-      float g = e.mods[(long)ri.req * e.mods_ld + e.gate_off + n];
+      const float g = e.mods[(long)row.req * e.mods_ld + e.gate_off + n];
       float* xo = (float*)e.out + (long)m * e.ldo + n;
       *xo = *xo + g * y;
       break;
@@ -80,24 +118,21 @@ __device__ __forceinline__ void epilogue_element(const EpiArgs& e, const BatchMe
       const int which = n / H;
       const int hn = n - which * H;
       const int h = hn / d, dd = hn - h * d;
-      RowInfo ri = row_info(meta, e.row_base + m);
-      const int p = padded_pos(meta, ri);
       float v = y;
-      if (which < 2 && ri.is_img) {
-        const int gw = meta.grid_w[ri.req];
+      if (which < 2 && row.gi >= 0) {
         const int half = d >> 1;
-        const int pos = (dd < half) ? (ri.local / gw) : (ri.local % gw);
+        const int pos = (dd < half) ? row.gi : row.gj;
         const int kk = (dd < half ? dd : dd - half) >> 1;
         const float2 cs = e.rope[pos * (d >> 2) + kk];
         // even: u cos - v sin ; odd: u sin + v cos  (u = even element, v = odd element)
         v = (dd & 1) ? (y_pair * cs.y + y * cs.x) : (y * cs.x - y_pair * cs.y);
       }
       if (which == 0)
-        ((T*)e.q)[((long)h * e.T + p) * d + dd] = from_f32<T>(v);
+        ((T*)e.q)[((long)h * e.T + row.pos) * d + dd] = from_f32<T>(v);
       else if (which == 1)
-        ((T*)e.k)[((long)h * e.T + p) * d + dd] = from_f32<T>(v);
+        ((T*)e.k)[((long)h * e.T + row.pos) * d + dd] = from_f32<T>(v);
       else
-        ((T*)e.vt)[((long)h * d + dd) * e.T + p] = from_f32<T>(v);
+        ((T*)e.vt)[((long)h * d + dd) * e.T + row.pos] = from_f32<T>(v);
       break;
     }
     default:

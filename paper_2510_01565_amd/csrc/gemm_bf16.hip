@@ -83,6 +83,8 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
   uint4 ra[A_CH], rb[B_CH];
   const int KT = (K + BK - 1) / BK;
 
+  // Global loads: addresses are clamped into the operand so every load is
+  // issued unconditionally; out-of-range chunks are replaced by zeros.
   auto gload = [&](int kt) {
     const int k0 = kt * BK;
 #pragma unroll
@@ -90,18 +92,18 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
       const int idx = tid + c * NT;
       const int row = idx >> 3, kc = idx & 7;
       const int gr = m0 + row, gk = k0 + kc * 8;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (gr < M && gk < K) v = *(const uint4*)(A + (long)gr * lda + gk);
-      ra[c] = v;
+      const bool ok = gr < M && gk < K;
+      const uint4 v = *(const uint4*)(A + (long)min(gr, M - 1) * lda + min(gk, K - 8));
+      ra[c] = ok ? v : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
     for (int c = 0; c < B_CH; ++c) {
       const int idx = tid + c * NT;
       const int row = idx >> 3, kc = idx & 7;
       const int gr = n0 + row, gk = k0 + kc * 8;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (gr < N && gk < K) v = *(const uint4*)(W + (long)gr * ldw + gk);
-      rb[c] = v;
+      const bool ok = gr < N && gk < K;
+      const uint4 v = *(const uint4*)(W + (long)min(gr, N - 1) * ldw + min(gk, K - 8));
+      rb[c] = ok ? v : make_uint4(0, 0, 0, 0);
     }
   };
   auto lstore = [&](int st) {
@@ -118,6 +120,21 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
       lds[st][(BM + row) * 8 + (kc ^ (row & 7))] = rb[c];
     }
   };
+  // fragments of k-step ks (16 wide) of stage st: lane row (lane & 31), chunk 2 ks + lane / 32
+  bf16x8_t fa[2][FM], fb[2][FN];
+  auto fload = [&](int st, int ks, int buf) {
+    const int ch = ks * 2 + (lane >> 5);
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int row = wm * WTM + i * 32 + (lane & 31);
+      fa[buf][i] = __builtin_bit_cast(bf16x8_t, lds[st][row * 8 + (ch ^ (row & 7))]);
+    }
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int row = wn * WTN + j * 32 + (lane & 31);
+      fb[buf][j] = __builtin_bit_cast(bf16x8_t, lds[st][(BM + row) * 8 + (ch ^ (row & 7))]);
+    }
+  };
 
   gload(0);
   lstore(0);
@@ -126,50 +143,53 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
   for (int kt = 0; kt < KT; ++kt) {
     const int st = kt & 1;
     if (kt + 1 < KT) gload(kt + 1);
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8_t a[FM], b[FN];
-      const int ch = ks * 2 + (lane >> 5);
-#pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        const int row = wm * WTM + i * 32 + (lane & 31);
-        uint4 u = lds[st][row * 8 + (ch ^ (row & 7))];
-        a[i] = __builtin_bit_cast(bf16x8_t, u);
-      }
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int row = wn * WTN + j * 32 + (lane & 31);
-        uint4 u = lds[st][(BM + row) * 8 + (ch ^ (row & 7))];
-        b[j] = __builtin_bit_cast(bf16x8_t, u);
-      }
+    fload(st, 0, 0);
+    static_for<BK / 16>([&](auto kk) {
+      constexpr int ks = decltype(kk)::value;
+      constexpr int cur = ks & 1;
+      if constexpr (ks + 1 < BK / 16) fload(st, ks + 1, cur ^ 1);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-    }
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j], 0, 0, 0);
+    });
     if (kt + 1 < KT) lstore(st ^ 1);
     __syncthreads();
   }
 
-  // epilogue: lane holds column (lane & 31) and rows (r/4)*8 + (lane/32)*4 + r%4 of each fragment
-  const EpiArgs& E = gi ? P.g[1].epi : P.g[0].epi;
+  // epilogue.  Row facts (request, joint position, grid position) are computed
+  // once per tile row into LDS, so the unrolled element loop never indexes the
+  // batch metadata.
+  RowEntry* rows = (RowEntry*)&lds[0][0];
+  static_assert(BM * sizeof(RowEntry) <= sizeof(lds), "row table");
+  const EpiArgs E = gi ? P.g[1].epi : P.g[0].epi;
+  if (E.mode == EPI_RESID || E.mode == EPI_QKV) {
+    for (int t = tid; t < BM; t += NT)
+      if (m0 + t < M) rows[t] = make_row_entry(P.meta, E.row_base + m0 + t);
+    __syncthreads();
+  }
   const bf16_t* bias = (const bf16_t*)E.bias;
-#pragma unroll
-  for (int j = 0; j < FN; ++j) {
+  static_for<FN>([&](auto jj) {
+    constexpr int j = decltype(jj)::value;
     const int n = n0 + wn * WTN + j * 32 + (lane & 31);
     const float bn = (bias != nullptr && n < N) ? bf2f(bias[n]) : 0.f;
-#pragma unroll
-    for (int i = 0; i < FM; ++i) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int m = m0 + wm * WTM + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+    static_for<FM>([&](auto ii) {
+      constexpr int i = decltype(ii)::value;
+      static_for<16>([&](auto rr) {
+        constexpr int r = decltype(rr)::value;
+        const int ml = wm * WTM + i * 32 + (r / 4) * 8 + (lane >> 5) * 4 + (r % 4);
+        const int m = m0 + ml;
         const float y = acc[i][j][r] + bn;
         const float yp = __shfl_xor(y, 1, 64);
-        if (m < M && n < N) epilogue_element<bf16_t>(E, P.meta, m, n, y, yp);
-      }
-    }
-  }
+        if (m < M && n < N) {
+          RowEntry re;
+          if (E.mode == EPI_RESID || E.mode == EPI_QKV) re = rows[ml];
+          epilogue_element<bf16_t>(E, re, m, n, y, yp);
+        }
+      });
+    });
+  });
 }
 
 template <int BM, int BN, int NWM, int NWN>

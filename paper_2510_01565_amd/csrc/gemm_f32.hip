@@ -61,12 +61,14 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmProblem P) {
     __syncthreads();
   }
 
-  const EpiArgs& E = gi ? P.g[1].epi : P.g[0].epi;
+  const EpiArgs E = gi ? P.g[1].epi : P.g[0].epi;
   const float* bias = (const float*)E.bias;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int m = m0 + ty * 4 + i;
     if (m >= M) continue;
+    RowEntry re;
+    if (E.mode == EPI_RESID || E.mode == EPI_QKV) re = make_row_entry(P.meta, E.row_base + m);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int n = n0 + tx * 4 + j;
@@ -75,7 +77,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmProblem P) {
       const int np = n0 + tx * 4 + jp;
       const float y = acc[i][j] + (bias ? bias[n] : 0.f);
       const float yp = acc[i][jp] + ((bias && np < N) ? bias[np] : 0.f);
-      epilogue_element<float>(E, P.meta, m, n, y, yp);
+      epilogue_element<float>(E, re, m, n, y, yp);
     }
   }
 }
