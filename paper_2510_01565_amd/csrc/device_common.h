@@ -140,6 +140,98 @@ __device__ __forceinline__ void epilogue_element(const EpiArgs& e, const RowEntr
   }
 }
 
+// 16 consecutive output columns n .. n+15 (n a multiple of 16) of one row m,
+// bias already added.  Vectorised form of epilogue_element: every store and
+// residual update is 16 bytes wide except the transposed V^T scatter.
+template <typename T>
+__device__ __forceinline__ void store16(T* dst, const float* v) {
+  if constexpr (sizeof(T) == 2) {
+    uint4 a, b;
+    a.x = pack_bf16x2(v[0], v[1]);
+    a.y = pack_bf16x2(v[2], v[3]);
+    a.z = pack_bf16x2(v[4], v[5]);
+    a.w = pack_bf16x2(v[6], v[7]);
+    b.x = pack_bf16x2(v[8], v[9]);
+    b.y = pack_bf16x2(v[10], v[11]);
+    b.z = pack_bf16x2(v[12], v[13]);
+    b.w = pack_bf16x2(v[14], v[15]);
+    ((uint4*)dst)[0] = a;
+    ((uint4*)dst)[1] = b;
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) ((float4*)dst)[q] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void epilogue_segment16(const EpiArgs& e, const RowEntry& row, int m, int n, float* v) {
+  switch (e.mode) {
+    case EPI_STORE_F32:
+      store16<float>((float*)e.out + (long)m * e.ldo + n, v);
+      break;
+    case EPI_STORE_T:
+      store16<T>((T*)e.out + (long)m * e.ldo + n, v);
+      break;
+    case EPI_GELU:
+#pragma unroll
+      for (int q = 0; q < 16; ++q) v[q] = gelu_tanh(v[q]);
+      store16<T>((T*)e.out + (long)m * e.ldo + e.col0 + n, v);
+      break;
+    case EPI_RESID: {
+      const float4* g = (const float4*)(e.mods + (long)row.req * e.mods_ld + e.gate_off + n);
+      float4* xo = (float4*)((float*)e.out + (long)m * e.ldo + n);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 gv = g[q];
+        float4 xv = xo[q];
+        xv.x += gv.x * v[4 * q];
+        xv.y += gv.y * v[4 * q + 1];
+        xv.z += gv.z * v[4 * q + 2];
+        xv.w += gv.w * v[4 * q + 3];
+        xo[q] = xv;
+      }
+      break;
+    }
+    case EPI_QKV: {
+      if (n >= e.n_qkv) {
+#pragma unroll
+        for (int q = 0; q < 16; ++q) v[q] = gelu_tanh(v[q]);
+        store16<T>((T*)e.gelu_out + (long)m * e.gelu_ld + e.gelu_col0 + (n - e.n_qkv), v);
+        break;
+      }
+      const int H = e.hidden, d = e.head_dim;
+      const int which = n / H;
+      const int hn = n - which * H;
+      const int h = hn / d, dd0 = hn - h * d;
+      if (which < 2 && row.gi >= 0) {
+        const int half = d >> 1;
+        const int pos = (dd0 < half) ? row.gi : row.gj;
+        const int k0 = (dd0 < half ? dd0 : dd0 - half) >> 1;
+        const float2* cs = e.rope + pos * (d >> 2) + k0;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const float2 c = cs[q];
+          const float u = v[2 * q], w = v[2 * q + 1];
+          v[2 * q] = u * c.x - w * c.y;
+          v[2 * q + 1] = u * c.y + w * c.x;
+        }
+      }
+      if (which == 0)
+        store16<T>((T*)e.q + ((long)h * e.T + row.pos) * d + dd0, v);
+      else if (which == 1)
+        store16<T>((T*)e.k + ((long)h * e.T + row.pos) * d + dd0, v);
+      else {
+        T* vt = (T*)e.vt + ((long)h * d + dd0) * e.T + row.pos;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) vt[(long)q * e.T] = from_f32<T>(v[q]);
+      }
+      break;
+    }
+    default:
+      break;
+  }
+}
+
 // XCD-aware block remap: hardware dispatches block b to XCD b % 8; return an
 // index such that every XCD owns one contiguous range of indices.
 __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
