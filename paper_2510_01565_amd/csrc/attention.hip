@@ -29,13 +29,24 @@ struct AttnSched {
   int tile_off[kMaxReq + 1]; // prefix sum of q-tiles per head
 };
 
-constexpr int BQ = 128;  // queries per block (4 waves x 32)
 constexpr int BKV = 64;  // keys per tile
 constexpr int D = 128;
+// Lazy rescaling: the running max used for exp2 is only raised when a new
+// score exceeds it by more than 2^RESCALE_SLACK; until then probabilities may
+// reach 2^8, which fp32 and bf16 hold exactly as well as any other value.
+// O and l always share the max they were computed with, so O / l is exact.
+constexpr float RESCALE_SLACK = 8.0f;
 
-__global__ __launch_bounds__(256) void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
-  __shared__ uint4 Ks[2][BKV * 16];  // [key][16 chunks of 8 d]
-  __shared__ uint4 Vs[2][D * 8];     // [d][8 chunks of 8 key slots]
+// NW waves x 32 queries per block.
+template <int NW>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW >= 8 ? 2 : 1)))
+void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
+  constexpr int NT = NW * 64;
+  constexpr int BQ = NW * 32;
+  constexpr int KCH = BKV * 16 / NT;  // 16-byte chunks of the K tile per thread
+  constexpr int VCH = D * 8 / NT;     // 16-byte chunks of the V^T tile per thread
+  __shared__ uint4 Ks[2][BKV * 16];  // [key][16 chunks of 8 d], chunk slot ^= key & 15
+  __shared__ uint4 Vs[2][D * 8];     // [d][8 chunks of 8 key slots], chunk slot ^= (d >> 1) & 7
 
   const int per_head = sc.tile_off[sc.n];
   const int id = xcd_remap(blockIdx.x, gridDim.x);
@@ -72,19 +83,19 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const AttnArgs a, const 
   float m_i = -INFINITY, l_i = 0.f;
   const float sl2 = a.scale * 1.4426950408889634f;
 
-  uint4 rk[4], rv[4];
+  uint4 rk[KCH], rv[VCH];
   auto gload = [&](int kv0) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int idx = tid + c * 256;
+    for (int c = 0; c < KCH; ++c) {
+      const int idx = tid + c * NT;
       const int row = idx >> 4, ch = idx & 15;
       uint4 u = make_uint4(0, 0, 0, 0);
       if (kv0 + row < L) u = *(const uint4*)(Kg + (long)(kv0 + row) * a.k_tok + ch * 8);
       rk[c] = u;
     }
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int idx = tid + c * 256;
+    for (int c = 0; c < VCH; ++c) {
+      const int idx = tid + c * NT;
       const int dr = idx >> 3, ch = idx & 7;
       const int key0 = kv0 + ch * 8;
       // padded V^T: the 8 columns are inside the buffer; columns >= L are zeroed
@@ -101,22 +112,23 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const AttnArgs a, const 
   };
   auto lstore = [&](int st) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int idx = tid + c * 256;
+    for (int c = 0; c < KCH; ++c) {
+      const int idx = tid + c * NT;
       const int row = idx >> 4, ch = idx & 15;
-      Ks[st][row * 16 + (ch ^ (row & 7))] = rk[c];
+      Ks[st][row * 16 + (ch ^ (row & 15))] = rk[c];
     }
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int idx = tid + c * 256;
+    for (int c = 0; c < VCH; ++c) {
+      const int idx = tid + c * NT;
       const int dr = idx >> 3, ch = idx & 7;
       // keys 8*ch .. 8*ch+7 = 16-key group g, half hf; slot order inside a group is
       // [0-3, 8-11, 4-7, 12-15] so lane half j reads its 8 keys as one 16-byte chunk
       const int g = ch >> 1, hf = ch & 1;
       uint2* row2 = (uint2*)&Vs[st][dr * 8];
       const int u_lo = g * 4 + hf, u_hi = g * 4 + 2 + hf;  // 8-byte units
-      row2[(((u_lo >> 1) ^ (dr & 7)) << 1) | (u_lo & 1)] = make_uint2(rv[c].x, rv[c].y);
-      row2[(((u_hi >> 1) ^ (dr & 7)) << 1) | (u_hi & 1)] = make_uint2(rv[c].z, rv[c].w);
+      const int sw = (dr >> 1) & 7;
+      row2[(((u_lo >> 1) ^ sw) << 1) | (u_lo & 1)] = make_uint2(rv[c].x, rv[c].y);
+      row2[(((u_hi >> 1) ^ sw) << 1) | (u_hi & 1)] = make_uint2(rv[c].z, rv[c].w);
     }
   };
 
@@ -141,7 +153,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const AttnArgs a, const 
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
         const int key = kb * 32 + (lane & 31);
-        const uint4 u = Ks[st][key * 16 + ((ks * 2 + hl) ^ (key & 7))];
+        const uint4 u = Ks[st][key * 16 + ((ks * 2 + hl) ^ (key & 15))];
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, u), qf[ks], s[kb], 0, 0, 0);
       }
     }
@@ -159,10 +171,17 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const AttnArgs a, const 
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kb][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_i, mx * sl2);
-    const float alpha = exp2f(m_i - m_new);
-    m_i = m_new;
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * sl2;
+    if (__any(mx > m_i + RESCALE_SLACK)) {
+      const float m_new = fmaxf(m_i, mx);
+      const float alpha = exp2f(m_i - m_new);
+      m_i = m_new;
+      l_i *= alpha;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
+    }
 
     float ls = 0.f;
     bf16x8_t pf[4];
@@ -170,22 +189,18 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const AttnArgs a, const 
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const float p = exp2f(fmaf(s[kb][i], sl2, -m_new));
+        const float p = exp2f(fmaf(s[kb][i], sl2, -m_i));
         ls += p;
         pf[kb * 2 + (i >> 3)][i & 7] = (__bf16)p;
       }
-    l_i = l_i * alpha + ls;
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
+    l_i += ls;
 
 #pragma unroll
     for (int ks2 = 0; ks2 < 4; ++ks2) {
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
         const int dr = db * 32 + (lane & 31);
-        const uint4 u = Vs[st][dr * 8 + ((ks2 * 2 + hl) ^ (dr & 7))];
+        const uint4 u = Vs[st][dr * 8 + ((ks2 * 2 + hl) ^ ((dr >> 1) & 7))];
         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, u), pf[ks2], o[db], 0, 0, 0);
       }
     }
@@ -309,13 +324,18 @@ AttnSched make_sched(const BatchMeta& m, int bq) {
 
 }  // namespace
 
-hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s) {
-  if (a.head_dim != D) return hipErrorInvalidValue;
-  const AttnSched sc = make_sched(a.meta, BQ);
+template <int NW>
+hipError_t launch_attn_nw(const AttnArgs& a, hipStream_t s) {
+  const AttnSched sc = make_sched(a.meta, NW * 32);
   const long blocks = (long)sc.tile_off[sc.n] * a.heads;
   if (blocks == 0) return hipSuccess;
-  hipLaunchKernelGGL(attn_bf16_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a, sc);
+  hipLaunchKernelGGL(attn_bf16_kernel<NW>, dim3((unsigned)blocks), dim3(NW * 64), 0, s, a, sc);
   return hipGetLastError();
+}
+
+hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s) {
+  if (a.head_dim != D) return hipErrorInvalidValue;
+  return launch_attn_nw<8>(a, s);
 }
 
 hipError_t launch_attention_f32(const AttnArgs& a, hipStream_t s) {
