@@ -107,21 +107,60 @@ def run_workload(torch, dit, synth, workloads, wl, cfg, w, steps, warmup, seed, 
     return res
 
 
-def roofline(kernels, dtype: str):
+KERNEL_SOURCES = {
+    "gemm_bf16": ["gemm_bf16.hip", "device_common.h", "dit_internal.h"],
+    "attention_bf16": ["attention.hip", "device_common.h", "dit_internal.h"],
+    "ln_modulate": ["elementwise.hip", "device_common.h", "dit_internal.h"],
+    "gemv": ["elementwise.hip", "device_common.h", "dit_internal.h"],
+}
+
+
+def kernel_source_hash(family: str) -> str:
+    """Hash of the sources a kernel family is built from (stale-counter check)."""
+    import hashlib
+    key = next((k for k in KERNEL_SOURCES if family.startswith(k)), None)
+    if key is None:
+        return ""
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[key]:
+        with open(os.path.join(ROOT, "paper_2510_01565_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(family: str, workload: str):
+    """HBM bytes per launch from the committed counter summary
+    profiles/hbm_traffic.txt (FETCH_SIZE and WRITE_SIZE passes, each scaled by
+    the same counter's reading for a plain copy of known size), or None when
+    no summary exists for this kernel, workload and kernel source."""
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    want = kernel_source_hash(family)
+    for line in open(path):
+        f = line.split()
+        if len(f) >= 4 and not line.startswith("#") and f[0] == family and f[1] == workload and f[2] == want:
+            return float(f[3])
+    return None
+
+
+def roofline(kernels, dtype: str, workload: str):
     """Dominant kernel family by time: algorithmic work per launch over its
     average launch duration (HIP events on the launch stream)."""
     name, k = max(kernels.items(), key=lambda kv: kv[1]["ms"])
     avg_ms = k["ms"] / k["launches"]
+    traffic = measured_traffic(name, workload)
     if k["flops"] > 0:
         peak = BF16_PEAK_TFLOPS if dtype == "bf16" else F32_PEAK_TFLOPS
         ach = k["flops"] / k["launches"] / (avg_ms / 1e3) / 1e12
         return {"kernel": name, "bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s",
-                "frac": ach / peak, "traffic": None, "launches_per_step": None, "avg_launch_ms": avg_ms,
-                "flop_per_launch": k["flops"] / k["launches"]}
+                "frac": ach / peak, "traffic": traffic, "avg_launch_ms": avg_ms,
+                "flop_per_launch": k["flops"] / k["launches"], "algorithmic_bytes_per_launch": k["bytes"] / k["launches"],
+                "launches": k["launches"]}
     ach = k["bytes"] / k["launches"] / (avg_ms / 1e3) / 1e9
     return {"kernel": name, "bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": ach / HBM_PEAK_GBS, "traffic": None, "avg_launch_ms": avg_ms,
-            "bytes_per_launch": k["bytes"] / k["launches"]}
+            "frac": ach / HBM_PEAK_GBS, "traffic": traffic, "avg_launch_ms": avg_ms,
+            "algorithmic_bytes_per_launch": k["bytes"] / k["launches"], "launches": k["launches"]}
 
 
 def cpu_baseline(wl, seed: int):
@@ -170,11 +209,14 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="dit57_1024px_bf16")
-    ap.add_argument("--extra", default="dit57_2048px_bf16,dit57_packed_mixed_bf16",
-                    help="comma-separated further workloads reported per resolution ('' for none)")
+    ap.add_argument("--extra", default="",
+                    help="comma-separated further workloads to report per resolution, e.g. "
+                         "dit57_2048px_bf16,dit57_packed_mixed_bf16 (each also has its own default run)")
     ap.add_argument("--extra-steps", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy-gib", type=float, default=0.0,
+                    help="first copy this many GiB device-to-device once (reference dispatch for HBM counters)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -188,6 +230,15 @@ def main() -> int:
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     dit.lib()
+    if args.calibrate_copy_gib > 0:
+        n = int(args.calibrate_copy_gib * 2 ** 30) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy: {n * 4} bytes read, {n * 4} bytes written")
+        del src, dst
     wl = workloads.WORKLOADS[args.workload]
     log(f"workload {wl.name}: {wl.note}")
     t0 = time.perf_counter()
@@ -207,7 +258,7 @@ def main() -> int:
         log(f"{name}: {r['ms_per_step']:.2f} ms/step, {r['tflops']:.1f} TFLOP/s ({100 * r['frac_peak']:.1f}% of peak)")
         per[name] = {k: v for k, v in r.items() if k != "kernels"}
 
-    rl = roofline(main_res["kernels"], wl.model.dtype)
+    rl = roofline(main_res["kernels"], wl.model.dtype, wl.name)
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
@@ -224,6 +275,9 @@ def main() -> int:
         "tflop_per_step": main_res["tflop_per_step"], "cv_pct": main_res["cv_pct"],
         "roofline": rl, "cpu_baseline": cpu, "per_workload": per,
         "kernels_ms_per_step": {k: round(v["ms_per_step"], 4) for k, v in main_res["kernels"].items()},
+        "kernels": {k: {"launches_per_step": v["launches"] // max(1, min(args.steps, 3)), "avg_launch_ms": v["ms"] / v["launches"],
+                        "tflops": v["flops"] / (v["ms"] / 1e3) / 1e12, "gbs": v["bytes"] / (v["ms"] / 1e3) / 1e9}
+                    for k, v in main_res["kernels"].items()},
     }
     print(json.dumps(out), flush=True)
     return 0
