@@ -1,19 +1,26 @@
 // bf16 GEMM on the gfx950 matrix cores: Y = A W^T + b, fp32 accumulation,
 // with the step's fused epilogues (QKV scatter + 2-D RoPE, GELU, gated
-// residual, plain stores).  Both operands are K-contiguous ([M, K] and
-// [N, K]), which is the layout v_mfma_f32_32x32x16_bf16 wants for its A and
-// B lanes (8 consecutive K values per lane), so tiles go global -> registers
-// -> LDS (16-byte chunks, XOR-swizzled per row against bank conflicts) ->
-// registers -> MFMA.  One launch may hold two problems ("groups") that share
-// N, e.g. the text and image streams of a double-stream block, so the small
-// text-stream GEMM fills otherwise idle compute units.
+// residual, plain stores).
+//
+// Both operands are K-contiguous ([M, K] and [N, K]), which is the layout
+// v_mfma_f32_32x32x16_bf16 wants for its A and B lanes (8 consecutive K values
+// per lane).  Tiles move global -> LDS -> registers -> MFMA:
+//  * when K is a multiple of the K tile, with direct-to-LDS loads
+//    (global_load_lds_dwordx4: each wave instruction writes 64 x 16 bytes of
+//    LDS without passing through registers) into a ring of STAGES buffers, so
+//    the loads of tile k + STAGES - 1 are in flight while tile k is multiplied;
+//  * otherwise through registers into two buffers, zero-filling the K tail.
+// LDS rows are XOR-swizzled per 16-byte chunk so that the 16 rows one
+// ds_read_b128 serves per cycle hit all 64 banks.  Blocks are remapped so
+// every XCD owns one contiguous range of output tiles (its L2 keeps the
+// operand panels those tiles share), in a grouped-M order.  One launch may
+// hold two problems ("groups") sharing N -- the text and image streams of a
+// double-stream block -- so the small text GEMM fills otherwise idle CUs.
 #include "device_common.h"
 
 namespace dit {
 
 namespace {
-
-constexpr int BK = 64;  // K per stage: 8 chunks of 8 bf16 per row
 
 struct TileCoord {
   int group, m0, n0;
@@ -45,24 +52,35 @@ __device__ __forceinline__ TileCoord tile_coord(const GemmProblem& P) {
   return c;
 }
 
-// LDS slot of 16-byte chunk `kc` (0..7) of tile row `row`: rows are 128 bytes,
-// the XOR spreads the rows that one ds_read_b128 serves together over all banks.
-template <int SWZ>
+// LDS slot (in 16-byte chunks) of chunk `kc` of tile row `row` for rows of
+// CPR chunks.  64 banks of 4 bytes serve 16 lanes of a ds_read_b128 per cycle:
+// the 16 consecutive rows read at one chunk index must cover all banks.
+template <int CPR>
 __device__ __forceinline__ int lds_slot(int row, int kc) {
-  if constexpr (SWZ == 0) return row * 8 + (kc ^ (row & 7));
-  else return row * 8 + (kc ^ ((row >> 1) & 7));
+  if constexpr (CPR == 8) return row * 8 + (kc ^ ((row >> 1) & 7));  // 128-byte rows: pairs of rows share 64 banks
+  else return row * 4 + (kc ^ ((row >> 2) & 3));                      // 64-byte rows: quads of rows share 64 banks
 }
 
-template <int BM, int BN, int NWM, int NWN, int SWZ = 1, int PF = 1, int PRIO = 0, int SGB = 0, int SB = 0>
+// s_waitcnt with vmcnt = n and the other counters left alone (gfx9 encoding:
+// vmcnt[3:0] and [15:14], expcnt[6:4], lgkmcnt[11:8]).
+template <int n>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(n >= 0 && n < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+template <int BM, int BN, int NWM, int NWN, int BK, int STAGES>
 __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProblem P) {
   constexpr int NT = NWM * NWN * 64;
+  constexpr int NWAVES = NWM * NWN;
   constexpr int WTM = BM / NWM, WTN = BN / NWN;
   constexpr int FM = WTM / 32, FN = WTN / 32;
-  constexpr int A_CH = BM * 8 / NT, B_CH = BN * 8 / NT;
-  static_assert(FM >= 1 && FN >= 1 && A_CH >= 1 && B_CH >= 1, "tile config");
-  static_assert((BM * 8) % NT == 0 && (BN * 8) % NT == 0, "tile config");
+  constexpr int CPR = BK / 8;                     // 16-byte chunks per tile row
+  constexpr int STAGE = (BM + BN) * CPR;          // uint4 per stage
+  static_assert(FM >= 1 && FN >= 1 && (BK == 32 || BK == 64) && STAGES >= 2, "tile config");
+  static_assert(STAGES * STAGE * 16 <= 160 * 1024, "LDS");
 
-  __shared__ uint4 lds[2][(BM + BN) * 8];
+  __shared__ uint4 lds[STAGES * STAGE];
 
   const TileCoord tc = tile_coord<BM, BN>(P);
   const int gi = tc.group;
@@ -88,62 +106,22 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // PF register sets of the next tiles: tile t is loaded into set t % PF
-  uint4 ra[PF][A_CH], rb[PF][B_CH];
   const int KT = (K + BK - 1) / BK;
 
-  // Global loads: addresses are clamped into the operand so every load is
-  // issued unconditionally; out-of-range chunks are replaced by zeros.
-  auto gload = [&](int kt, auto set) {
-    constexpr int S = decltype(set)::value;
-    const int k0 = kt * BK;
-#pragma unroll
-    for (int c = 0; c < A_CH; ++c) {
-      const int idx = tid + c * NT;
-      const int row = idx >> 3, kc = idx & 7;
-      const int gr = m0 + row, gk = k0 + kc * 8;
-      const bool ok = gr < M && gk < K;
-      const uint4 v = *(const uint4*)(A + (long)min(gr, M - 1) * lda + min(gk, K - 8));
-      ra[S][c] = ok ? v : make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int c = 0; c < B_CH; ++c) {
-      const int idx = tid + c * NT;
-      const int row = idx >> 3, kc = idx & 7;
-      const int gr = n0 + row, gk = k0 + kc * 8;
-      const bool ok = gr < N && gk < K;
-      const uint4 v = *(const uint4*)(W + (long)min(gr, N - 1) * ldw + min(gk, K - 8));
-      rb[S][c] = ok ? v : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto lstore = [&](int st, auto set) {
-    constexpr int S = decltype(set)::value;
-#pragma unroll
-    for (int c = 0; c < A_CH; ++c) {
-      const int idx = tid + c * NT;
-      const int row = idx >> 3, kc = idx & 7;
-      lds[st][lds_slot<SWZ>(row, kc)] = ra[S][c];
-    }
-#pragma unroll
-    for (int c = 0; c < B_CH; ++c) {
-      const int idx = tid + c * NT;
-      const int row = idx >> 3, kc = idx & 7;
-      lds[st][lds_slot<SWZ>(BM + row, kc)] = rb[S][c];
-    }
-  };
   // fragments of k-step ks (16 wide) of stage st: lane row (lane & 31), chunk 2 ks + lane / 32
   bf16x8_t fa[2][FM], fb[2][FN];
   auto fload = [&](int st, int ks, int buf) {
     const int ch = ks * 2 + (lane >> 5);
+    const uint4* S = lds + st * STAGE;
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
       const int row = wm * WTM + i * 32 + (lane & 31);
-      fa[buf][i] = __builtin_bit_cast(bf16x8_t, lds[st][lds_slot<SWZ>(row, ch)]);
+      fa[buf][i] = __builtin_bit_cast(bf16x8_t, S[lds_slot<CPR>(row, ch)]);
     }
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
       const int row = wn * WTN + j * 32 + (lane & 31);
-      fb[buf][j] = __builtin_bit_cast(bf16x8_t, lds[st][lds_slot<SWZ>(BM + row, ch)]);
+      fb[buf][j] = __builtin_bit_cast(bf16x8_t, S[lds_slot<CPR>(BM + row, ch)]);
     }
   };
   auto compute = [&](int st) {
@@ -152,48 +130,109 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
       constexpr int ks = decltype(kk)::value;
       constexpr int cur = ks & 1;
       if constexpr (ks + 1 < BK / 16) fload(st, ks + 1, cur ^ 1);
-      // SB: keep the next k-step's fragment reads ahead of this k-step's MFMAs
-      if constexpr (SB) __builtin_amdgcn_sched_barrier(0);
-      if constexpr (PRIO) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j], 0, 0, 0);
-      if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
-      if constexpr (SB) __builtin_amdgcn_sched_barrier(0);
-      if constexpr (SGB) {
-        // one fragment read of the next k-step between consecutive MFMAs
-        constexpr int NR = (ks + 1 < BK / 16) ? FM + FN : 0;
-        static_for<NR>([&](auto) {
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        });
-        __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - NR, 0);
-      }
     });
   };
-  // one K tile: prefetch tile kt + PF into the set that held tile kt, compute
-  // tile kt from LDS, then stage tile kt + 1 into the other LDS buffer
-  auto iter = [&](int kt, auto set) {
-    constexpr int S = decltype(set)::value;
-    if (kt + PF < KT) gload(kt + PF, set);
-    compute(kt & 1);
-    if (kt + 1 < KT) lstore((kt + 1) & 1, std::integral_constant<int, (S + 1) % PF>{});
-    __syncthreads();
-  };
 
-  gload(0, std::integral_constant<int, 0>{});
-  if constexpr (PF > 1)
-    if (KT > 1) gload(1, std::integral_constant<int, 1 % PF>{});
-  lstore(0, std::integral_constant<int, 0>{});
-  __syncthreads();
-  if constexpr (PF == 1) {
-    for (int kt = 0; kt < KT; ++kt) iter(kt, std::integral_constant<int, 0>{});
+  if (K % BK == 0) {
+    // ---- direct-to-LDS ring.  Wave instruction q of a tile moves 64 lanes x 16
+    // bytes = RPI tile rows; lane l fills slot l % CPR of row l / CPR and so
+    // fetches the logical chunk that the swizzle puts in that slot.  Rows past
+    // M / N are clamped (their products only reach discarded outputs).
+    constexpr int RPI = 64 / CPR;                       // tile rows per instruction
+    constexpr int AI = BM / RPI / NWAVES, BI = BN / RPI / NWAVES;
+    static_assert(AI * RPI * NWAVES == BM && BI * RPI * NWAVES == BN, "tile config");
+    constexpr int IPT = AI + BI;                        // load instructions per tile per wave
+    auto dtl_load = [&](int kt, int st) {
+      const int k0 = kt * BK;
+      const int lr = lane / CPR, sl = lane % CPR;
+      uint4* S = lds + st * STAGE;
+#pragma unroll
+      for (int q = 0; q < AI; ++q) {
+        const int r0 = (wave * AI + q) * RPI, row = r0 + lr;
+        const int kc = lds_slot<CPR>(row, sl) - row * CPR;  // the XOR is an involution
+        const bf16_t* g = A + (long)min(m0 + row, M - 1) * lda + k0 + kc * 8;
+        __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)(S + r0 * CPR), 16,
+                                         0, 0);
+      }
+#pragma unroll
+      for (int q = 0; q < BI; ++q) {
+        const int r0 = (wave * BI + q) * RPI, row = r0 + lr;
+        const int kc = lds_slot<CPR>(BM + row, sl) - (BM + row) * CPR;
+        const bf16_t* g = W + (long)min(n0 + row, N - 1) * ldw + k0 + kc * 8;
+        __builtin_amdgcn_global_load_lds((const void*)g,
+                                         (__attribute__((address_space(3))) void*)(S + (BM + r0) * CPR), 16, 0, 0);
+      }
+    };
+    // prologue: tiles 0 .. STAGES-2 in flight
+#pragma unroll
+    for (int t = 0; t < STAGES - 1; ++t)
+      if (t < KT) dtl_load(t, t);
+    for (int kt = 0; kt < KT; ++kt) {
+      // own loads of tile kt complete (later tiles may stay in flight), then
+      // every wave's: after the barrier tile kt is in LDS and every wave has
+      // finished tile kt - 1, whose buffer the next load reuses
+      const int after = min(KT - 1, kt + STAGES - 2) - kt;
+      static_for<STAGES - 1>([&](auto aa) {
+        constexpr int a = decltype(aa)::value;
+        if (after == a) wait_vmcnt<a * IPT>();
+      });
+      __syncthreads();
+      if (kt + STAGES - 1 < KT) dtl_load(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
+      compute(kt % STAGES);
+    }
+    __syncthreads();
   } else {
-    for (int kt = 0; kt < KT; kt += 2) {
-      iter(kt, std::integral_constant<int, 0>{});
-      if (kt + 1 < KT) iter(kt + 1, std::integral_constant<int, 1>{});
+    // ---- register path with zero-filled K tail (two LDS buffers).
+    constexpr int A_CH = BM * CPR / NT, B_CH = BN * CPR / NT;
+    static_assert((BM * CPR) % NT == 0 && (BN * CPR) % NT == 0 && A_CH >= 1 && B_CH >= 1, "tile config");
+    uint4 ra[A_CH], rb[B_CH];
+    auto gload = [&](int kt) {
+      const int k0 = kt * BK;
+#pragma unroll
+      for (int c = 0; c < A_CH; ++c) {
+        const int idx = tid + c * NT;
+        const int row = idx / CPR, kc = idx % CPR;
+        const int gr = m0 + row, gk = k0 + kc * 8;
+        const bool ok = gr < M && gk < K;
+        const uint4 v = *(const uint4*)(A + (long)min(gr, M - 1) * lda + min(gk, K - 8));
+        ra[c] = ok ? v : make_uint4(0, 0, 0, 0);
+      }
+#pragma unroll
+      for (int c = 0; c < B_CH; ++c) {
+        const int idx = tid + c * NT;
+        const int row = idx / CPR, kc = idx % CPR;
+        const int gr = n0 + row, gk = k0 + kc * 8;
+        const bool ok = gr < N && gk < K;
+        const uint4 v = *(const uint4*)(W + (long)min(gr, N - 1) * ldw + min(gk, K - 8));
+        rb[c] = ok ? v : make_uint4(0, 0, 0, 0);
+      }
+    };
+    auto lstore = [&](int st) {
+      uint4* S = lds + st * STAGE;
+#pragma unroll
+      for (int c = 0; c < A_CH; ++c) {
+        const int idx = tid + c * NT;
+        S[lds_slot<CPR>(idx / CPR, idx % CPR)] = ra[c];
+      }
+#pragma unroll
+      for (int c = 0; c < B_CH; ++c) {
+        const int idx = tid + c * NT;
+        S[lds_slot<CPR>(BM + idx / CPR, idx % CPR)] = rb[c];
+      }
+    };
+    gload(0);
+    lstore(0);
+    __syncthreads();
+    for (int kt = 0; kt < KT; ++kt) {
+      if (kt + 1 < KT) gload(kt + 1);
+      compute(kt & 1);
+      if (kt + 1 < KT) lstore((kt + 1) & 1);
+      __syncthreads();
     }
   }
 
@@ -202,10 +241,10 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
   // metadata.  Each 32x32 accumulator fragment is staged through a per-wave
   // LDS buffer so that a lane ends up with 16 consecutive columns of one row
   // and stores them with 16-byte writes.
-  RowEntry* rows = (RowEntry*)&lds[0][0];
+  RowEntry* rows = (RowEntry*)&lds[0];
   constexpr int SP = 36;  // staging row pitch in floats (16-byte aligned rows)
-  float* stg = (float*)&lds[0][0] + BM * (sizeof(RowEntry) / 4) + wave * 32 * SP;
-  static_assert(BM * sizeof(RowEntry) + NWM * NWN * 32 * SP * 4 <= sizeof(lds), "epilogue LDS");
+  float* stg = (float*)&lds[0] + BM * (sizeof(RowEntry) / 4) + wave * 32 * SP;
+  static_assert(BM * sizeof(RowEntry) + NWAVES * 32 * SP * 4 <= sizeof(lds), "epilogue LDS");
   const EpiArgs E = gi ? P.g[1].epi : P.g[0].epi;
   const bool need_rows = E.mode == EPI_RESID || E.mode == EPI_QKV;
   if (need_rows) {
@@ -252,20 +291,17 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
   });
 }
 
-template <int BM, int BN, int NWM, int NWN, int SWZ = 1, int PF = 1, int PRIO = 0, int SGB = 0, int SB = 0>
+template <int BM, int BN, int NWM, int NWN, int BK, int STAGES>
 hipError_t launch_cfg(const GemmProblem& p, hipStream_t s) {
   const int tiles_n = (p.N + BN - 1) / BN;
   long tiles = (long)((p.g[0].M + BM - 1) / BM) * tiles_n;
   if (p.n_groups > 1) tiles += (long)((p.g[1].M + BM - 1) / BM) * tiles_n;
   if (tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, NWM, NWN, SWZ, PF, PRIO, SGB, SB>), dim3((unsigned)tiles), dim3(NWM * NWN * 64), 0, s,
-                     p);
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, NWM, NWN, BK, STAGES>), dim3((unsigned)tiles), dim3(NWM * NWN * 64), 0,
+                     s, p);
   return hipGetLastError();
 }
 
-}  // namespace
-
-namespace {
 enum GemmCfg { CFG_128x64 = 0, CFG_256x256 = 1, CFG_128x128 = 2 };
 GemmCfg pick(const GemmProblem& p) {
   int maxM = p.g[0].M;
@@ -274,6 +310,7 @@ GemmCfg pick(const GemmProblem& p) {
   if (maxM >= 1024 && p.N >= 1024) return CFG_256x256;
   return CFG_128x128;
 }
+
 }  // namespace
 
 const char* gemm_bf16_config_name(const GemmProblem& p) {
@@ -284,11 +321,11 @@ const char* gemm_bf16_config_name(const GemmProblem& p) {
 hipError_t launch_gemm_bf16(const GemmProblem& p, hipStream_t s) {
   switch (pick(p)) {
     case CFG_128x64:
-      return launch_cfg<128, 64, 4, 1>(p, s);
+      return launch_cfg<128, 64, 4, 1, 64, 2>(p, s);
     case CFG_256x256:
-      return launch_cfg<256, 256, 2, 4>(p, s);
+      return launch_cfg<256, 256, 2, 4, 64, 2>(p, s);
     default:
-      return launch_cfg<128, 128, 2, 2>(p, s);
+      return launch_cfg<128, 128, 2, 2, 64, 2>(p, s);
   }
 }
 
