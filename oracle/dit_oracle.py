@@ -267,11 +267,17 @@ def _p(params, name, dtype):
 
 
 def double_block(params, cfg: OracleConfig, i: int, x_txt: np.ndarray, x_img: np.ndarray,
-                 c: np.ndarray, grid_hw: Tuple[int, int], dtype=F64):
+                 c: np.ndarray, grid_hw: Tuple[int, int], dtype=F64,
+                 rows_txt: Optional[np.ndarray] = None, rows_img: Optional[np.ndarray] = None):
     """Double-stream (MMDiT) block on one request: each stream has its own
-    weights and modulation; attention is joint over [text; image]."""
+    weights and modulation; attention is joint over [text; image].
+    ``rows_txt`` / ``rows_img`` select the output rows to compute (all by
+    default); keys and values always come from every token."""
     H, nh, d, eps = cfg.hidden, cfg.heads, cfg.head_dim, cfg.ln_eps
     x = {"txt": np.asarray(x_txt, dtype), "img": np.asarray(x_img, dtype)}
+    Lt, Li = x["txt"].shape[0], x["img"].shape[0]
+    sel = {"txt": np.arange(Lt) if rows_txt is None else np.asarray(rows_txt),
+           "img": np.arange(Li) if rows_img is None else np.asarray(rows_img)}
     mkey = {s: f"double.{i}.{'img' if cfg.tie_streams else s}" for s in ("txt", "img")}
     mods = {s: modulation(params, cfg, mkey[s], c, dtype) for s in ("txt", "img")}
     q, k, v = {}, {}, {}
@@ -287,42 +293,50 @@ def double_block(params, cfg: OracleConfig, i: int, x_txt: np.ndarray, x_img: np
     gh, gw = grid_hw
     q["img"] = rope_2d(q["img"], gh, gw, cfg.rope_theta)
     k["img"] = rope_2d(k["img"], gh, gw, cfg.rope_theta)
-    Lt = x["txt"].shape[0]
+    joint_rows = np.concatenate([sel["txt"], Lt + sel["img"]])
     o = attention(np.concatenate([q["txt"], q["img"]]), np.concatenate([k["txt"], k["img"]]),
-                  np.concatenate([v["txt"], v["img"]]))
+                  np.concatenate([v["txt"], v["img"]]), rows=joint_rows)
     o = o.reshape(o.shape[0], H)
-    o_s = {"txt": o[:Lt], "img": o[Lt:]}
+    nt = len(sel["txt"])
+    o_s = {"txt": o[:nt], "img": o[nt:]}
+    out = {}
     for s in ("txt", "img"):
         pre = stream_prefix(cfg, i, s)
         _, _, g1, sh2, sc2, g2 = mods[s]
-        x[s] = x[s] + g1 * linear(o_s[s], _p(params, pre + "proj.w", dtype), _p(params, pre + "proj.b", dtype))
-        hmid = gelu_tanh(linear(modulate(x[s], sh2, sc2, eps),
+        xs = x[s][sel[s]]
+        xs = xs + g1 * linear(o_s[s], _p(params, pre + "proj.w", dtype), _p(params, pre + "proj.b", dtype))
+        hmid = gelu_tanh(linear(modulate(xs, sh2, sc2, eps),
                                 _p(params, pre + "mlp1.w", dtype), _p(params, pre + "mlp1.b", dtype)))
-        x[s] = x[s] + g2 * linear(hmid, _p(params, pre + "mlp2.w", dtype), _p(params, pre + "mlp2.b", dtype))
-    return x["txt"], x["img"]
+        out[s] = xs + g2 * linear(hmid, _p(params, pre + "mlp2.w", dtype), _p(params, pre + "mlp2.b", dtype))
+    return out["txt"], out["img"]
 
 
 def single_block(params, cfg: OracleConfig, i: int, x: np.ndarray, n_txt: int,
-                 c: np.ndarray, grid_hw: Tuple[int, int], dtype=F64) -> np.ndarray:
+                 c: np.ndarray, grid_hw: Tuple[int, int], dtype=F64,
+                 rows: Optional[np.ndarray] = None) -> np.ndarray:
     """Single-stream block on one request's joint sequence x = [text; image]:
     one linear produces Q, K, V and the MLP input; attention and GELU(MLP)
-    are concatenated and projected by a second linear; one gated residual."""
+    are concatenated and projected by a second linear; one gated residual.
+    ``rows`` selects the output rows to compute (all by default)."""
     H, nh, d, eps = cfg.hidden, cfg.heads, cfg.head_dim, cfg.ln_eps
     x = np.asarray(x, dtype)
+    L = x.shape[0]
+    sel = np.arange(L) if rows is None else np.asarray(rows)
     sh, sc, g = modulation(params, cfg, f"single.{i}", c, dtype)
     pre = f"single.{i}."
-    z = linear(modulate(x, sh, sc, eps), _p(params, pre + "lin1.w", dtype), _p(params, pre + "lin1.b", dtype))
-    L = z.shape[0]
-    q = z[:, 0:H].reshape(L, nh, d)
-    k = z[:, H:2 * H].reshape(L, nh, d)
-    v = z[:, 2 * H:3 * H].reshape(L, nh, d)
+    w1, b1 = _p(params, pre + "lin1.w", dtype), _p(params, pre + "lin1.b", dtype)
+    a = modulate(x, sh, sc, eps)
+    zq = linear(a, w1[:3 * H], b1[:3 * H])          # Q, K, V of every token
+    q = zq[:, 0:H].reshape(L, nh, d)
+    k = zq[:, H:2 * H].reshape(L, nh, d)
+    v = zq[:, 2 * H:3 * H].reshape(L, nh, d)
     gh, gw = grid_hw
     q = np.concatenate([q[:n_txt], rope_2d(q[n_txt:], gh, gw, cfg.rope_theta)])
     k = np.concatenate([k[:n_txt], rope_2d(k[n_txt:], gh, gw, cfg.rope_theta)])
-    o = attention(q, k, v).reshape(L, H)
-    mlp = gelu_tanh(z[:, 3 * H:])
+    o = attention(q, k, v, rows=sel).reshape(len(sel), H)
+    mlp = gelu_tanh(linear(a[sel], w1[3 * H:], b1[3 * H:]))
     y = linear(np.concatenate([o, mlp], axis=1), _p(params, pre + "lin2.w", dtype), _p(params, pre + "lin2.b", dtype))
-    return x + g * y
+    return x[sel] + g * y
 
 
 def conditioning(params, cfg: OracleConfig, t: float, dtype=F64) -> np.ndarray:

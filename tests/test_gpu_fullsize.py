@@ -1,0 +1,194 @@
+"""Parity at the full workload sizes, in the launch configurations the
+benchmark times: outputs the oracle can compute one by one are sampled (GEMM
+elements, attention rows, block rows), and whole 57-block steps are checked
+through properties that hold at any size (packed = unpacked, determinism)."""
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2510_01565_amd import dit, synth, workloads
+from harness import BF16_TOL, F32_TOL, normwise_err, oracle_cfg
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dev(seed, name, shape, std, dtype):
+    torch = _torch()
+    return synth.device_normal(seed, name, shape, std, dtype, torch.device("cuda"))
+
+
+def _host64(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def _rows(n, extra, rng, k=12):
+    base = [r for r in extra if 0 <= r < n]
+    return np.unique(np.concatenate([np.array(base, dtype=np.int64), rng.integers(0, n, k)]))
+
+
+@pytest.mark.parametrize("M,N,K", [(4608, 21504, 3072), (4608, 3072, 15360), (4096, 12288, 3072), (512, 9216, 3072),
+                                   (16896, 9216, 3072)])
+def test_linear_real_shapes_sampled(M, N, K):
+    """The step's GEMM shapes (1024 px single-stream linear1 / linear2, MLP up,
+    text QKV, 2048 px QKV): 600 sampled outputs against fp64 dot products."""
+    torch = _torch()
+    x = _dev(7, "x", (M, K), 1.0, torch.bfloat16)
+    w = _dev(7, "w", (N, K), 0.02, torch.bfloat16)
+    b = _dev(7, "b", (N,), 0.02, torch.bfloat16)
+    y = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    dit.dit_linear(M, N, K, dit.DIT_BF16, x, w, b, y, dit.DIT_F32)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(M + N + K)
+    ms = np.concatenate([[0, M - 1, 255, 256], rng.integers(0, M, 596)])
+    ns = np.concatenate([[0, N - 1, 255, 256], rng.integers(0, N, 596)])
+    xs = _host64(x[torch.from_numpy(ms).cuda()])
+    ws = _host64(w[torch.from_numpy(ns).cuda()])
+    ref = (xs * ws).sum(axis=1) + _host64(b)[ns]
+    got = y[torch.from_numpy(ms).cuda(), torch.from_numpy(ns).cuda()].cpu().numpy()
+    assert normwise_err(got, ref) < F32_TOL
+
+
+def _attention_case(grids, n_txt, heads, seed, rows_per_req):
+    torch = _torch()
+    lens = [g * g + t for g, t in zip(grids, n_txt)]
+    T = sum(lens)
+    d = 128
+    q = _dev(seed, "q", (T, heads, d), 1.0, torch.bfloat16)
+    k = _dev(seed, "k", (T, heads, d), 1.0, torch.bfloat16)
+    v = _dev(seed, "v", (T, heads, d), 1.0, torch.bfloat16)
+    b = dit.Batch(grids, grids, n_txt)
+    nws = dit.attention_workspace_size(b, heads, d, dit.DIT_BF16)
+    ws = torch.empty(nws, dtype=torch.uint8, device="cuda")
+    o = torch.empty_like(q)
+    dit.dit_attention(b, heads, d, dit.DIT_BF16, q, k, v, o, ws, nws)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(seed)
+    off = 0
+    for L, extra in zip(lens, rows_per_req):
+        rows = _rows(L, extra, rng)
+        sl = slice(off, off + L)
+        ref = O.attention(_host64(q[sl]), _host64(k[sl]), _host64(v[sl]), rows=rows)
+        got = o[off + torch.from_numpy(rows).cuda()].float().cpu().numpy()
+        assert normwise_err(got, ref) < BF16_TOL, L
+        off += L
+
+
+def test_attention_sp4_share_2048px_sampled():
+    """One GPU's share of the 4-way split at 2048 px: 6 of 24 heads over the
+    whole 16896-token sequence (512 text + 16384 image tokens)."""
+    edge = [0, 1, 255, 256, 511, 512, 513, 8191, 8192, 16895, 16832, 16831]
+    _attention_case([128], [512], 6, 11, [edge])
+
+
+def test_attention_packed_mixed_sampled():
+    """The packed 256/512/1024/2048 px batch, 24 heads, block-diagonal."""
+    grids = [16, 32, 64, 128]
+    lens = [g * g + 512 for g in grids]
+    edge = [[0, L - 1, 511, 512, 255, 256] for L in lens]
+    _attention_case(grids, [512] * 4, 24, 12, edge)
+
+
+def _block_weights(m, seed):
+    torch = _torch()
+    cfg = dit.make_config(m)
+    shapes = dit.weight_manifest(cfg)
+    dev = [synth.device_normal(seed, "w:" + n, s, synth.WEIGHT_STD, torch.bfloat16, torch.device("cuda"))
+           for n, s in shapes]
+    return cfg, shapes, dev
+
+
+def _host_params(shapes, dev, names):
+    return {n: t.float().cpu().numpy() for (n, _), t in zip(shapes, dev) if n in names or n.startswith(names)}
+
+
+def test_double_block_1024px_sampled_rows():
+    """Double-stream block at the 1024 px shape (512 text + 4096 image tokens,
+    3072 wide): sampled output rows of both streams against the oracle."""
+    torch = _torch()
+    m = workloads.FLUX_DOUBLE
+    cfg, shapes, dev = _block_weights(m, 21)
+    H = m.hidden
+    x = _dev(21, "hidden", (512 + 4096, H), 1.0, torch.bfloat16).float()
+    c = _dev(21, "cond", (1, H), 1.0, torch.float32)
+    x_host = x.cpu().numpy().astype(np.float64)
+    b = dit.Batch([64], [64], [512], [0.5])
+    nws = dit.workspace_size(cfg, b)
+    ws = torch.empty(nws, dtype=torch.uint8, device="cuda")
+    dit.dit_block_forward(cfg, dit.Weights(dev), 0, 0, b, x, c, ws, nws)
+    torch.cuda.synchronize()
+    got = x.cpu().numpy()
+    params = _host_params(shapes, dev, ("double.0.", "mod."))
+    rng = np.random.default_rng(21)
+    rt = _rows(512, [0, 255, 256, 511], rng)
+    ri = _rows(4096, [0, 63, 64, 2047, 4095], rng)
+    ot, oi = O.double_block(params, oracle_cfg(m), 0, x_host[:512], x_host[512:], c.cpu().numpy()[0].astype(np.float64),
+                            (64, 64), rows_txt=rt, rows_img=ri)
+    assert normwise_err(got[rt], ot) < BF16_TOL
+    assert normwise_err(got[512 + ri], oi) < BF16_TOL
+
+
+def test_single_block_1024px_sampled_rows():
+    """Single-stream block at the 1024 px shape: linear1 (Q, K, V + RoPE and
+    GELU-MLP in one GEMM), attention, linear2 with the gated residual."""
+    torch = _torch()
+    m = workloads.ModelShape(hidden=3072, heads=24, head_dim=128, mlp_ratio=4, n_double=0, n_single=1,
+                             in_channels=64, text_dim=4096)
+    cfg, shapes, dev = _block_weights(m, 22)
+    H = m.hidden
+    x = _dev(22, "hidden", (512 + 4096, H), 1.0, torch.bfloat16).float()
+    c = _dev(22, "cond", (1, H), 1.0, torch.float32)
+    x_host = x.cpu().numpy().astype(np.float64)
+    b = dit.Batch([64], [64], [512], [0.5])
+    nws = dit.workspace_size(cfg, b)
+    ws = torch.empty(nws, dtype=torch.uint8, device="cuda")
+    dit.dit_block_forward(cfg, dit.Weights(dev), 1, 0, b, x, c, ws, nws)
+    torch.cuda.synchronize()
+    got = x.cpu().numpy()
+    params = _host_params(shapes, dev, ("single.0.", "mod."))
+    rng = np.random.default_rng(22)
+    rows = _rows(4608, [0, 511, 512, 513, 4607, 2560], rng)
+    ref = O.single_block(params, oracle_cfg(m), 0, x_host, 512, c.cpu().numpy()[0].astype(np.float64), (64, 64),
+                         rows=rows)
+    assert normwise_err(got[rows], ref) < BF16_TOL
+
+
+def test_full_step_packed_equals_unpacked_and_deterministic():
+    """The 57-block model on the packed 256/512/1024/2048 px batch (the
+    benchmark's packed workload): the packed velocity equals each request
+    stepped alone, bit for bit, and two runs agree bit for bit."""
+    torch = _torch()
+    wl = workloads.WORKLOADS["dit57_packed_mixed_bf16"]
+    m = wl.model
+    cfg, _, dev = _block_weights(m, 0)
+    w = dit.Weights(dev)
+    grids = wl.grids()
+    ts = [float(t) for t in synth.uniform(0, "timesteps:" + wl.name, (4,))]
+    lat = _dev(0, "latents", (sum(wl.n_img()), m.in_channels), 1.0, torch.bfloat16)
+    txt = _dev(0, "text", (sum(wl.n_txt), m.text_dim), 1.0, torch.bfloat16)
+
+    def step(gs, nt, tt, la, tx):
+        b = dit.Batch(gs, gs, nt, tt)
+        nws = dit.workspace_size(cfg, b)
+        ws = torch.empty(nws, dtype=torch.uint8, device="cuda")
+        v = torch.empty_like(la)
+        dit.dit_step(cfg, w, b, la, tx, v, ws, nws)
+        torch.cuda.synchronize()
+        return v
+
+    packed = step(grids, wl.n_txt, ts, lat, txt)
+    again = step(grids, wl.n_txt, ts, lat, txt)
+    assert torch.isfinite(packed.float()).all().item()
+    assert packed.float().abs().max().item() > 0
+    assert torch.equal(packed.view(torch.int16), again.view(torch.int16))
+    io = to = 0
+    for r, g in enumerate(grids):
+        n = g * g
+        one = step([g], [512], [ts[r]], lat[io:io + n].contiguous(), txt[to:to + 512].contiguous())
+        assert torch.equal(one.view(torch.int16), packed[io:io + n].view(torch.int16)), g
+        io += n
+        to += 512

@@ -333,3 +333,18 @@ def test_step_is_per_request():
     v1, x1 = O.dit_step(p, cfg, reqs[1:], [0.2])
     np.testing.assert_array_equal(vs[1], v1[0])
     np.testing.assert_array_equal(xs[1], reqs[1].latents - 0.2 * vs[1])
+
+
+def test_sampled_rows_match_full_blocks():
+    p = _tiny(seed=6)
+    rng = np.random.default_rng(13)
+    xt, xi, c = rng.standard_normal((5, 32)), rng.standard_normal((12, 32)), rng.standard_normal(32)
+    yt, yi = O.double_block(p, TINY, 0, xt, xi, c, (3, 4))
+    rt, ri = np.array([4, 0]), np.array([11, 3, 7])
+    st, si = O.double_block(p, TINY, 0, xt, xi, c, (3, 4), rows_txt=rt, rows_img=ri)
+    np.testing.assert_allclose(st, yt[rt], rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(si, yi[ri], rtol=1e-13, atol=1e-13)
+    x = np.concatenate([xt, xi])
+    y = O.single_block(p, TINY, 0, x, 5, c, (3, 4))
+    rows = np.array([16, 2, 9])
+    np.testing.assert_allclose(O.single_block(p, TINY, 0, x, 5, c, (3, 4), rows=rows), y[rows], rtol=1e-13, atol=1e-13)
