@@ -174,7 +174,7 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * sl2;
     if (__any(mx > m_i + RESCALE_SLACK)) {
       const float m_new = fmaxf(m_i, mx);
-      const float alpha = exp2f(m_i - m_new);
+      const float alpha = __builtin_amdgcn_exp2f(m_i - m_new);
       m_i = m_new;
       l_i *= alpha;
 #pragma unroll
@@ -189,7 +189,9 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const float p = exp2f(fmaf(s[kb][i], sl2, -m_i));
+        // v_exp_f32 directly: results below 2^-126 flush to zero, which the
+        // softmax sum and the bf16 probabilities cannot tell from their true value
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[kb][i], sl2, -m_i));
         ls += p;
         pf[kb * 2 + (i >> 3)][i & 7] = (__bf16)p;
       }

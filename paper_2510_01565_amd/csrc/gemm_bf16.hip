@@ -323,7 +323,7 @@ hipError_t launch_gemm_bf16(const GemmProblem& p, hipStream_t s) {
     case CFG_128x64:
       return launch_cfg<128, 64, 4, 1, 64, 2>(p, s);
     case CFG_256x256:
-      return launch_cfg<256, 256, 2, 4, 64, 2>(p, s);
+      return launch_cfg<256, 256, 4, 2, 64, 2>(p, s);
     default:
       return launch_cfg<128, 128, 2, 2, 64, 2>(p, s);
   }

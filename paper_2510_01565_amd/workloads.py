@@ -70,7 +70,8 @@ WORKLOADS = {
         note="19 double + 38 single blocks, 512 text + 16384 image tokens, bf16"),
     "dit57_2048px_sp4_share_bf16": Workload(
         "dit57_2048px_sp4_share_bf16", FLUX_FULL, [2048], [512], t=[0.5], kind="attention_share",
-        note="one GPU's share of a 4-way sequence-parallel split: 6 of 24 heads over 16896 tokens"),
+        note="one GPU's share of a 4-way sequence-parallel split: 6 of 24 heads over 16896 tokens",
+        extra={"sp": 4}),
     "dit57_packed_mixed_bf16": Workload(
         "dit57_packed_mixed_bf16", FLUX_FULL, [256, 512, 1024, 2048], [512, 512, 512, 512], t=None,
         note="4 requests 256/512/1024/2048 px packed, per-request timesteps U[0,1)"),
