@@ -37,16 +37,40 @@ constexpr int D = 128;
 // O and l always share the max they were computed with, so O / l is exact.
 constexpr float RESCALE_SLACK = 8.0f;
 
+// Scheduling pattern for a run of N (LDS read, MFMA) pairs where MFMA i uses
+// read i: the first A reads, then one MFMA and one read alternately, then the
+// last A MFMAs -- A fragment reads stay in flight ahead of the matrix cores.
+template <int N, int A>
+__device__ __forceinline__ void sched_read_ahead() {
+  __builtin_amdgcn_sched_group_barrier(0x100, A, 0);
+  static_for<N - A>([&](auto) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  });
+  __builtin_amdgcn_sched_group_barrier(0x008, A, 0);
+}
+
+// s_waitcnt with vmcnt = 0 and the other counters left alone (gfx9 encoding).
+__device__ __forceinline__ void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); }
+
 // NW waves x 32 queries per block.
+//
+// Pipeline over 64-key tiles j: K and V^T tiles arrive by direct-to-LDS loads
+// (global_load_lds_dwordx4) in a ring of 3 buffers, issued two tiles ahead.
+// Inside a wave the score MFMAs of tile j + 1 are issued before the softmax
+// of tile j, so the matrix cores work on S(j + 1) while the vector ALUs
+// exponentiate tile j; then P(j) V(j) accumulates into O.
 template <int NW>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW >= 8 ? 2 : 1)))
 void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
-  constexpr int NT = NW * 64;
   constexpr int BQ = NW * 32;
-  constexpr int KCH = BKV * 16 / NT;  // 16-byte chunks of the K tile per thread
-  constexpr int VCH = D * 8 / NT;     // 16-byte chunks of the V^T tile per thread
-  __shared__ uint4 Ks[2][BKV * 16];  // [key][16 chunks of 8 d], chunk slot ^= key & 15
-  __shared__ uint4 Vs[2][D * 8];     // [d][8 chunks of 8 key slots], chunk slot ^= (d >> 1) & 7
+  constexpr int STAGES = 3;
+  constexpr int KT_U4 = BKV * 16;  // K tile: [64 keys][16 chunks of 8 d], chunk slot ^= key & 15
+  constexpr int VT_U4 = D * 8;     // V^T tile: [128 d][8 chunks of 8 key slots], chunk slot ^= (d >> 1) & 7
+  constexpr int KI = BKV / 4 / NW; // K-tile load instructions per wave (4 keys each)
+  constexpr int VI = D / 8 / NW;   // V^T-tile load instructions per wave (8 rows each)
+  static_assert(KI * 4 * NW == BKV && VI * 8 * NW == D, "tile config");
+  __shared__ uint4 smem[STAGES][KT_U4 + VT_U4];
 
   const int per_head = sc.tile_off[sc.n];
   const int id = xcd_remap(blockIdx.x, gridDim.x);
@@ -64,6 +88,33 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
   const bf16_t* __restrict__ Qg = (const bf16_t*)a.q + (long)a.qk_off[r] * a.q_tok + (long)h * a.q_head;
   const bf16_t* __restrict__ Kg = (const bf16_t*)a.k + (long)a.qk_off[r] * a.k_tok + (long)h * a.k_head;
   const bf16_t* __restrict__ Vg = (const bf16_t*)a.vt + (long)a.vt_off[r] + (long)h * a.vt_head;
+
+  // K rows past L are clamped to the last key (their scores are masked); V^T
+  // columns past L are in the request's padding, which holds zeros.
+  auto tile_load = [&](int j, int st) {
+    const int kv0 = j * BKV;
+    uint4* S = smem[st];
+#pragma unroll
+    for (int q = 0; q < KI; ++q) {
+      const int k0 = (wave * KI + q) * 4;
+      const int key = k0 + (lane >> 4), sl = lane & 15;
+      const bf16_t* g = Kg + (long)min(kv0 + key, L - 1) * a.k_tok + (sl ^ (key & 15)) * 8;
+      __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)(S + k0 * 16), 16, 0,
+                                       0);
+    }
+#pragma unroll
+    for (int q = 0; q < VI; ++q) {
+      const int d0 = (wave * VI + q) * 8;
+      const int dr = d0 + (lane >> 3), sl = lane & 7;
+      const bf16_t* g = Vg + (long)dr * a.vt_d + kv0 + (sl ^ ((dr >> 1) & 7)) * 8;
+      __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)(S + KT_U4 + d0 * 8),
+                                       16, 0, 0);
+    }
+  };
+
+  const int ntiles = (L + BKV - 1) / BKV;
+  tile_load(0, 0);
+  if (ntiles > 1) tile_load(1, 1);
 
   // Q fragments (B operand of S^T = K Q^T): query q0 + wave*32 + lane%32, d chunk 2*ks + lane/32
   const int qrow = q0 + wave * 32 + (lane & 31);
@@ -83,67 +134,10 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
   float m_i = -INFINITY, l_i = 0.f;
   const float sl2 = a.scale * 1.4426950408889634f;
 
-  uint4 rk[KCH], rv[VCH];
-  auto gload = [&](int kv0) {
-#pragma unroll
-    for (int c = 0; c < KCH; ++c) {
-      const int idx = tid + c * NT;
-      const int row = idx >> 4, ch = idx & 15;
-      uint4 u = make_uint4(0, 0, 0, 0);
-      if (kv0 + row < L) u = *(const uint4*)(Kg + (long)(kv0 + row) * a.k_tok + ch * 8);
-      rk[c] = u;
-    }
-#pragma unroll
-    for (int c = 0; c < VCH; ++c) {
-      const int idx = tid + c * NT;
-      const int dr = idx >> 3, ch = idx & 7;
-      const int key0 = kv0 + ch * 8;
-      // padded V^T: the 8 columns are inside the buffer; columns >= L are zeroed
-      uint4 u = *(const uint4*)(Vg + (long)dr * a.vt_d + key0);
-      if (key0 + 8 > L) {
-        uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (key0 + e >= L) w[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
-        u = make_uint4(w[0], w[1], w[2], w[3]);
-      }
-      rv[c] = u;
-    }
-  };
-  auto lstore = [&](int st) {
-#pragma unroll
-    for (int c = 0; c < KCH; ++c) {
-      const int idx = tid + c * NT;
-      const int row = idx >> 4, ch = idx & 15;
-      Ks[st][row * 16 + (ch ^ (row & 15))] = rk[c];
-    }
-#pragma unroll
-    for (int c = 0; c < VCH; ++c) {
-      const int idx = tid + c * NT;
-      const int dr = idx >> 3, ch = idx & 7;
-      // keys 8*ch .. 8*ch+7 = 16-key group g, half hf; slot order inside a group is
-      // [0-3, 8-11, 4-7, 12-15] so lane half j reads its 8 keys as one 16-byte chunk
-      const int g = ch >> 1, hf = ch & 1;
-      uint2* row2 = (uint2*)&Vs[st][dr * 8];
-      const int u_lo = g * 4 + hf, u_hi = g * 4 + 2 + hf;  // 8-byte units
-      const int sw = (dr >> 1) & 7;
-      row2[(((u_lo >> 1) ^ sw) << 1) | (u_lo & 1)] = make_uint2(rv[c].x, rv[c].y);
-      row2[(((u_hi >> 1) ^ sw) << 1) | (u_hi & 1)] = make_uint2(rv[c].z, rv[c].w);
-    }
-  };
-
-  const int ntiles = (L + BKV - 1) / BKV;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-
-  for (int it = 0; it < ntiles; ++it) {
-    const int st = it & 1;
-    const int kv0 = it * BKV;
-    if (it + 1 < ntiles) gload(kv0 + BKV);
-
-    // S^T for 64 keys x 32 queries: two 32x32 blocks
-    f32x16_t s[2];
+  // S^T of one 64-key tile: two 32x32 blocks (keys kb*32 + (i/4)*8 + hl*4 + i%4 of
+  // register i, query lane % 32)
+  auto scores = [&](int st, f32x16_t* s) {
+    const uint4* S = smem[st];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -153,10 +147,16 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
         const int key = kb * 32 + (lane & 31);
-        const uint4 u = Ks[st][key * 16 + ((ks * 2 + hl) ^ (key & 15))];
+        const uint4 u = S[key * 16 + ((ks * 2 + hl) ^ (key & 15))];
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, u), qf[ks], s[kb], 0, 0, 0);
       }
     }
+    // keep four fragment reads ahead of the MFMAs that consume them
+    sched_read_ahead<2 * D / 16, 4>();
+  };
+  // online softmax of tile j's scores, then O += P V
+  auto softmax_pv = [&](int j, int st, f32x16_t* s) {
+    const int kv0 = j * BKV;
     if (kv0 + BKV > L) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
@@ -182,7 +182,6 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
     }
-
     float ls = 0.f;
     bf16x8_t pf[4];
 #pragma unroll
@@ -196,18 +195,37 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
         pf[kb * 2 + (i >> 3)][i & 7] = (__bf16)p;
       }
     l_i += ls;
-
+    const uint4* V = smem[st] + KT_U4;
 #pragma unroll
     for (int ks2 = 0; ks2 < 4; ++ks2) {
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
         const int dr = db * 32 + (lane & 31);
-        const uint4 u = Vs[st][dr * 8 + ((ks2 * 2 + hl) ^ ((dr >> 1) & 7))];
+        const uint4 u = V[dr * 8 + ((ks2 * 2 + hl) ^ ((dr >> 1) & 7))];
         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, u), pf[ks2], o[db], 0, 0, 0);
       }
     }
-    if (it + 1 < ntiles) lstore(st ^ 1);
+    sched_read_ahead<4 * D / 32, 4>();
+  };
+  // one pipeline step: tile j's scores are in s_cur
+  // (after the last tile the scores of a nonexistent tile j + 1 are computed
+  // from a stale buffer and discarded: no branch separates them from the softmax)
+  auto step = [&](int j, f32x16_t* s_cur, f32x16_t* s_nxt) {
+    // tile j + 1 resident for every wave; every wave is done with tile j - 1
+    wait_vmcnt0();
     __syncthreads();
+    if (j + 2 < ntiles) tile_load(j + 2, (j + 2) % STAGES);
+    scores((j + 1) % STAGES, s_nxt);
+    softmax_pv(j, j % STAGES, s_cur);
+  };
+
+  f32x16_t sa[2], sb[2];
+  wait_vmcnt0();
+  __syncthreads();
+  scores(0, sa);
+  for (int j = 0; j < ntiles; j += 2) {
+    step(j, sa, sb);
+    if (j + 1 < ntiles) step(j + 1, sb, sa);
   }
 
   const float l = l_i + __shfl_xor(l_i, 32, 64);
@@ -270,7 +288,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const AttnArgs a, const At
     for (int idx = tid; idx < 64 * FD; idx += 64) {
       const int c = idx / 64, kr = idx % 64;
       const bool ok = kv0 + kr < L;
-      Vsh[kr][c] = ok ? Vg[(long)c * a.vt_d + kv0 + kr] : 0.f;
+      Vsh[kr][c] = ok ? Vg[(long)c * a.vt_d + vt_slot(kv0 + kr)] : 0.f;
     }
     __syncthreads();
     const int nk = min(64, L - kv0);

@@ -634,6 +634,8 @@ dit_status dit_step(const dit_config* cfg, const dit_weights* w, const dit_batch
   // conditioning: c = W2 SiLU(W1 e(t) + b1) + b2; all modulation vectors m = Wm SiLU(c) + bm
   HIP_TRY(timed(x.s, "setup", 0.0, 0.0, [&] { return launch_rope_table(x.ws.rope, x.L.d, cfg->rope_theta, x.s); }));
   HIP_TRY(timed(x.s, "setup", 0.0, 0.0,
+                [&] { return launch_vt_pad_zero(dt, x.ws.Vt, meta, x.L.heads, x.L.d, x.s); }));
+  HIP_TRY(timed(x.s, "setup", 0.0, 0.0,
                 [&] { return launch_timestep_embed(x.ws.temb, n, batch->t, cfg->time_freq_dim, x.s); }));
   HIP_TRY(gemv(x.s, dt, Wt(x, 0), Wt(x, 1), x.ws.temb, cfg->time_freq_dim, n, cfg->time_freq_dim, H, 0, x.ws.u, H));
   HIP_TRY(gemv(x.s, dt, Wt(x, 2), Wt(x, 3), x.ws.u, H, n, H, H, 1, x.ws.cvec, H));
@@ -698,6 +700,8 @@ dit_status dit_block_forward(const dit_config* cfg, const dit_weights* w, int ki
   x.es = elem_size(cfg->dtype);
   const int H = x.L.H, n = meta.n_req;
   HIP_TRY(timed(x.s, "setup", 0.0, 0.0, [&] { return launch_rope_table(x.ws.rope, x.L.d, cfg->rope_theta, x.s); }));
+  HIP_TRY(timed(x.s, "setup", 0.0, 0.0,
+                [&] { return launch_vt_pad_zero(cfg->dtype, x.ws.Vt, meta, x.L.heads, x.L.d, x.s); }));
   if (kind == 0) {
     // this block's modulation rows: image stream, then (untied) text stream
     const int off = x.L.mod_dbl(index, 0);
@@ -762,6 +766,7 @@ dit_status dit_attention(const dit_batch* batch, int heads, int head_dim, int dt
   hipStream_t s = (hipStream_t)stream;
   HIP_TRY(timed(s, "v_transpose", 0.0, 2.0 * m.T * heads * head_dim * elem_size(dtype),
                 [&] { return launch_v_transpose(dtype, v, m, heads, head_dim, ws, s); }));
+  HIP_TRY(timed(s, "v_transpose", 0.0, 0.0, [&] { return launch_vt_pad_zero(dtype, ws, m, heads, head_dim, s); }));
   AttnArgs a;
   memset(&a, 0, sizeof(a));
   const long Tp = m.pad_off[m.n_req];

@@ -60,6 +60,11 @@ __host__ __device__ inline int padded_pos(const BatchMeta& m, const RowInfo& ri)
   return m.pad_off[ri.req] + (ri.is_img ? m.n_txt[ri.req] : 0) + ri.local;
 }
 
+// Column of padded position `pos` in V^T.  Inside every aligned group of 16
+// keys the middle two quads are swapped (keys 4-7 <-> 8-11), the order in
+// which one 32x32 score fragment holds them; an involution.
+__host__ __device__ inline int vt_slot(int pos) { return (pos & ~12) | ((pos & 4) << 1) | ((pos & 8) >> 1); }
+
 // joint position -> stream-major row
 __host__ __device__ inline int joint_to_row(const BatchMeta& m, int p) {
   int r = 0;
@@ -93,7 +98,7 @@ struct EpiArgs {
   // EPI_QKV
   void* q;              // [heads][T][d]
   void* k;              // [heads][T][d]
-  void* vt;             // [heads][d][T]
+  void* vt;             // [heads][d][T], column vt_slot(padded position)
   int T;                // padded joint length (pad_off[n_req])
   int hidden;
   int head_dim;
@@ -165,8 +170,10 @@ hipError_t launch_ln_modulate(int out_dtype, const float* X, int H, int row_begi
                               long ldo, hipStream_t s);
 hipError_t launch_euler(int dtype, void* x, const void* v, int channels, const BatchMeta& meta,
                         const float* dt_host, hipStream_t s);
-// v [T_joint, heads, d] (joint order) -> vt [heads][d][pad_off[n]] at padded columns
+// v [T_joint, heads, d] (joint order) -> vt [heads][d][pad_off[n]] at columns vt_slot(padded position)
 hipError_t launch_v_transpose(int dtype, const void* v, const BatchMeta& meta, int heads, int d, void* vt,
                               hipStream_t s);
+// zeroes the V^T columns of the padding keys of every request (padded positions >= the request length)
+hipError_t launch_vt_pad_zero(int dtype, void* vt, const BatchMeta& meta, int heads, int d, hipStream_t s);
 
 }  // namespace dit

@@ -200,13 +200,33 @@ __global__ void v_transpose_kernel(const T* __restrict__ v, const BatchMeta meta
     if (p < T_ && dd < d) {
       int r = 0;
       while (r + 1 < meta.n_req && p >= meta.joint_off[r + 1]) ++r;
-      const int col = meta.pad_off[r] + (p - meta.joint_off[r]);
+      const int col = vt_slot(meta.pad_off[r] + (p - meta.joint_off[r]));
       vt[((long)h * d + dd) * ld + col] = tile[tx][yy];
     }
   }
 }
 
+template <typename T>
+__global__ void vt_pad_zero_kernel(T* __restrict__ vt, const BatchMeta meta, long ld) {
+  const long row = blockIdx.x;  // h * d + dd
+  for (int r = 0; r < meta.n_req; ++r) {
+    const int L = meta.joint_off[r + 1] - meta.joint_off[r];
+    const int P = meta.pad_off[r + 1] - meta.pad_off[r];
+    for (int k = L + threadIdx.x; k < P; k += blockDim.x) vt[row * ld + vt_slot(meta.pad_off[r] + k)] = T(0);
+  }
+}
+
 }  // namespace
+
+hipError_t launch_vt_pad_zero(int dtype, void* vt, const BatchMeta& meta, int heads, int d, hipStream_t s) {
+  const long ld = meta.pad_off[meta.n_req];
+  const dim3 grid((unsigned)(heads * d));
+  if (dtype == DIT_BF16)
+    hipLaunchKernelGGL(vt_pad_zero_kernel<bf16_t>, grid, dim3(64), 0, s, (bf16_t*)vt, meta, ld);
+  else
+    hipLaunchKernelGGL(vt_pad_zero_kernel<float>, grid, dim3(64), 0, s, (float*)vt, meta, ld);
+  return hipGetLastError();
+}
 
 hipError_t launch_rope_table(float2* table, int head_dim, float theta, hipStream_t s) {
   const int quarter = head_dim / 4;
