@@ -144,10 +144,69 @@ def measured_traffic(family: str, workload: str):
     return None
 
 
+def run_sp_share(torch, dit, synth, workloads, wl, cfg, w, steps, seed, dev):
+    """One GPU's share of a k-way (Ulysses) sequence-parallel step at real shape,
+    composed from measured launches: every non-attention kernel of a step on
+    the rank's token shard (L/k tokens: n_txt/k text + grid^2/k image), plus
+    one attention per block over all L tokens for n_heads/k heads -- the
+    all-to-alls between them are not part of a one-GPU measurement."""
+    k = wl.extra.get("sp", 4)
+    m = wl.model
+    g = wl.grids()[0]
+    shard_grid = (g // k, g) if g % k == 0 else (g, g)
+    n_txt_shard = wl.n_txt[0] // k
+    b = dit.Batch([shard_grid[0]], [shard_grid[1]], [n_txt_shard], [0.5])
+    nws = dit.workspace_size(cfg, b)
+    ws = torch.empty(nws, dtype=torch.uint8, device=dev)
+    lat = synth.device_normal(seed, "latents:share", (shard_grid[0] * shard_grid[1], m.in_channels), 1.0, torch.bfloat16, dev)
+    txt = synth.device_normal(seed, "text:share", (n_txt_shard, m.text_dim), 1.0, torch.bfloat16, dev)
+    vel = torch.empty_like(lat)
+    stream = torch.cuda.current_stream()
+    for _ in range(2):
+        dit.dit_step(cfg, w, b, lat, txt, vel, ws, nws, stream)
+    torch.cuda.synchronize()
+    dit.profile_start()
+    for _ in range(steps):
+        dit.dit_step(cfg, w, b, lat, txt, vel, ws, nws, stream)
+        dit.euler_update(b, m.in_channels, dit.DIT_BF16, lat, vel, [wl.dt], stream)
+    torch.cuda.synchronize()
+    kern = dit.profile_stop()
+    non_attn_ms = sum(v["ms"] for n, v in kern.items()
+                      if not n.startswith("attention") and not n.startswith("detail:")) / steps
+    # attention of the rank's heads over the whole sequence
+    heads = m.heads // k
+    L = wl.n_txt[0] + g * g
+    ab = dit.Batch([g], [g], [wl.n_txt[0]])
+    q = synth.device_normal(seed, "share.q", (L, heads, m.head_dim), 1.0, torch.bfloat16, dev)
+    kk = synth.device_normal(seed, "share.k", (L, heads, m.head_dim), 1.0, torch.bfloat16, dev)
+    v = synth.device_normal(seed, "share.v", (L, heads, m.head_dim), 1.0, torch.bfloat16, dev)
+    o = torch.empty_like(q)
+    anws = dit.attention_workspace_size(ab, heads, m.head_dim, dit.DIT_BF16)
+    aws = torch.empty(anws, dtype=torch.uint8, device=dev)
+    dit.dit_attention(ab, heads, m.head_dim, dit.DIT_BF16, q, kk, v, o, aws, anws, stream)
+    torch.cuda.synchronize()
+    nblk = m.n_double + m.n_single
+    dit.profile_start()
+    for _ in range(nblk):
+        dit.dit_attention(ab, heads, m.head_dim, dit.DIT_BF16, q, kk, v, o, aws, anws, stream)
+    torch.cuda.synchronize()
+    akern = dit.profile_stop()
+    attn_ms = sum(x["ms"] for n, x in akern.items() if n.startswith("attention"))
+    share_ms = non_attn_ms + attn_ms
+    fl = workloads.flops_per_step(m, [n_txt_shard], [shard_grid[0] * shard_grid[1]])
+    attn_flops = nblk * 4.0 * L * L * m.head_dim * heads
+    total = fl["gemm"] + attn_flops
+    return {"steps_per_s": 1e3 / share_ms, "ms_per_step": share_ms, "non_attention_ms": non_attn_ms,
+            "attention_ms": attn_ms, "tflop_per_step": total / 1e12, "tflops": total / (share_ms / 1e3) / 1e12,
+            "frac_peak": total / (share_ms / 1e3) / 1e12 / BF16_PEAK_TFLOPS,
+            "note": f"composed: non-attention kernels of a step on the {L // k}-token shard + {nblk} attention "
+                    f"launches of {heads} heads over {L} tokens (HIP events); all-to-alls excluded"}
+
+
 def roofline(kernels, dtype: str, workload: str):
     """Dominant kernel family by time: algorithmic work per launch over its
     average launch duration (HIP events on the launch stream)."""
-    name, k = max(kernels.items(), key=lambda kv: kv[1]["ms"])
+    name, k = max(((n, v) for n, v in kernels.items() if not n.startswith("detail:")), key=lambda kv: kv[1]["ms"])
     avg_ms = k["ms"] / k["launches"]
     traffic = measured_traffic(name, workload)
     if k["flops"] > 0:
@@ -251,7 +310,14 @@ def main() -> int:
     per = {wl.name: {k: v for k, v in main_res.items() if k != "kernels"}}
     for name in [x for x in args.extra.split(",") if x]:
         ow = workloads.WORKLOADS[name]
-        if ow.model != wl.model or ow.kind != "step":
+        if ow.model != wl.model:
+            continue
+        if ow.kind == "attention_share":
+            r = run_sp_share(torch, dit, synth, workloads, ow, cfg, w, args.extra_steps, args.seed, dev)
+            log(f"{name}: {r['ms_per_step']:.2f} ms per share step, {r['tflops']:.1f} TFLOP/s ({r['note']})")
+            per[name] = r
+            continue
+        if ow.kind != "step":
             continue
         r = run_workload(torch, dit, synth, workloads, ow, cfg, w, args.extra_steps, 1, args.seed, dev,
                          profile=False)
@@ -274,10 +340,13 @@ def main() -> int:
         "tflops": main_res["tflops"], "frac_bf16_peak": main_res["frac_peak"],
         "tflop_per_step": main_res["tflop_per_step"], "cv_pct": main_res["cv_pct"],
         "roofline": rl, "cpu_baseline": cpu, "per_workload": per,
-        "kernels_ms_per_step": {k: round(v["ms_per_step"], 4) for k, v in main_res["kernels"].items()},
+        "kernels_ms_per_step": {k: round(v["ms_per_step"], 4) for k, v in main_res["kernels"].items()
+                                if not k.startswith("detail:")},
         "kernels": {k: {"launches_per_step": v["launches"] // max(1, min(args.steps, 3)), "avg_launch_ms": v["ms"] / v["launches"],
                         "tflops": v["flops"] / (v["ms"] / 1e3) / 1e12, "gbs": v["bytes"] / (v["ms"] / 1e3) / 1e9}
-                    for k, v in main_res["kernels"].items()},
+                    for k, v in main_res["kernels"].items() if not k.startswith("detail:")},
+        "gemm_shapes": {k[7:]: {"ms_per_step": round(v["ms_per_step"], 4), "tflops": round(v["flops"] / (v["ms"] / 1e3) / 1e12, 1)}
+                        for k, v in main_res["kernels"].items() if k.startswith("detail:")},
     }
     print(json.dumps(out), flush=True)
     return 0

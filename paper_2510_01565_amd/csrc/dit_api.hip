@@ -51,7 +51,7 @@ struct ProfRecord {
   double flops, bytes;
 };
 struct Profiler {
-  std::mutex mu;
+  std::recursive_mutex mu;  // timed() nests for the per-shape detail entries
   bool on = false;
   std::vector<hipEvent_t> pool;
   size_t used = 0;
@@ -80,7 +80,7 @@ template <class F>
 hipError_t timed(hipStream_t s, const char* family, double flops, double bytes, F&& launch) {
   Profiler& P = prof();
   if (!P.on) return launch();
-  std::lock_guard<std::mutex> lock(P.mu);
+  std::lock_guard<std::recursive_mutex> lock(P.mu);
   int fi = -1;
   for (size_t i = 0; i < P.fams.size(); ++i)
     if (P.fams[i].name == family) fi = (int)i;
@@ -315,11 +315,29 @@ double gemm_bytes(const GemmProblem& p, int es) {
   return b;
 }
 
+const char* epi_name(int mode) {
+  static const char* n[] = {"store_f32", "store", "gelu", "resid", "qkv"};
+  return (mode >= 0 && mode <= 4) ? n[mode] : "?";
+}
+
 hipError_t gemm(hipStream_t s, int dtype, const GemmProblem& p) {
   const int es = dtype == DIT_BF16 ? 2 : 4;
-  if (dtype == DIT_BF16)
-    return timed(s, gemm_bf16_config_name(p), gemm_flops(p), gemm_bytes(p, es),
-                 [&] { return launch_gemm_bf16(p, s); });
+  if (dtype == DIT_BF16) {
+    if (!prof().on)
+      return launch_gemm_bf16(p, s);
+    // kernel family for the roofline, plus a per-shape entry ("detail:" prefix)
+    // that splits the same launches by N, K and epilogue
+    char detail[160];
+    int M = p.g[0].M + (p.n_groups > 1 ? p.g[1].M : 0);
+    snprintf(detail, sizeof(detail), "detail:%s M=%d N=%d K=%d %s", gemm_bf16_config_name(p), M, p.N, p.g[0].K,
+             epi_name(p.g[0].epi.mode));
+    hipError_t e = hipSuccess;
+    hipError_t r = timed(s, detail, gemm_flops(p), gemm_bytes(p, es), [&] {
+      e = timed(s, gemm_bf16_config_name(p), gemm_flops(p), gemm_bytes(p, es), [&] { return launch_gemm_bf16(p, s); });
+      return e;
+    });
+    return r != hipSuccess ? r : e;
+  }
   return timed(s, "gemm_f32", gemm_flops(p), gemm_bytes(p, es), [&] { return launch_gemm_f32(p, s); });
 }
 
@@ -823,7 +841,7 @@ dit_status dit_linear(int M, int N, int K, int dtype, const void* x, const void*
 dit_status dit_profile_start(void) {
   g_err.clear();
   Profiler& P = prof();
-  std::lock_guard<std::mutex> lock(P.mu);
+  std::lock_guard<std::recursive_mutex> lock(P.mu);
   P.recs.clear();
   P.fams.clear();
   P.used = 0;
@@ -834,7 +852,7 @@ dit_status dit_profile_start(void) {
 dit_status dit_profile_stop(int* n_families) {
   g_err.clear();
   Profiler& P = prof();
-  std::lock_guard<std::mutex> lock(P.mu);
+  std::lock_guard<std::recursive_mutex> lock(P.mu);
   P.on = false;
   for (const ProfRecord& r : P.recs) {
     float ms = 0.f;
@@ -856,7 +874,7 @@ dit_status dit_profile_entry(int i, const char** family, long* launches, double*
                              double* bytes) {
   g_err.clear();
   Profiler& P = prof();
-  std::lock_guard<std::mutex> lock(P.mu);
+  std::lock_guard<std::recursive_mutex> lock(P.mu);
   if (i < 0 || i >= (int)P.fams.size()) return fail(DIT_ERR_INVALID_ARG, "family %d out of range", i);
   const ProfFamily& f = P.fams[i];
   if (family) *family = f.name.c_str();

@@ -136,6 +136,20 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
         for (int j = 0; j < FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j], 0, 0, 0);
     });
+    // Instruction order for the scheduler: the first k-step's fragment reads,
+    // then each k-step's MFMAs alternating with the next k-step's reads, so
+    // LDS latency hides under the matrix cores inside every wave.
+    constexpr int NR = FM + FN, NM = FM * FN, NP = NR < NM ? NR : NM;
+    __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);  // DS read
+    static_for<BK / 16 - 1>([&](auto) {
+      static_for<NP>([&](auto) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      });
+      if constexpr (NM > NP) __builtin_amdgcn_sched_group_barrier(0x008, NM - NP, 0);
+      if constexpr (NR > NP) __builtin_amdgcn_sched_group_barrier(0x100, NR - NP, 0);
+    });
+    __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
   };
 
   if (K % BK == 0) {
