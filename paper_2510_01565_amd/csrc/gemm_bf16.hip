@@ -273,12 +273,42 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
     const int nb = n0 + wn * WTN + j * 32;
     const int nl = nb + (lane & 31);
     const float bn = (bias != nullptr && nl < N) ? bf2f(bias[nl]) : 0.f;
+    // V^T columns of a QKV epilogue: a lane takes one column and 16 consecutive
+    // rows, which (when they are 16 consecutive, 16-aligned joint positions of
+    // one request) land in one aligned 16-key group of V^T: two 16-byte stores.
+    const bool vcols = E.mode == EPI_QKV && nb >= 2 * E.hidden && nb < 3 * E.hidden;
     static_for<FM>([&](auto ii) {
       constexpr int i = decltype(ii)::value;
       static_for<16>([&](auto rr) {
         constexpr int r = decltype(rr)::value;
         stg[((r / 4) * 8 + (lane >> 5) * 4 + (r % 4)) * SP + (lane & 31)] = acc[i][j][r] + bn;
       });
+      if (vcols) {
+        const int rh = lane >> 5, c = lane & 31;
+        float v[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) v[q] = stg[(rh * 16 + q) * SP + c];
+        const int ml0 = wm * WTM + i * 32 + rh * 16;
+        const int m = m0 + ml0, n = nb + c;
+        if (n < N && m < M) {
+          const RowEntry r0 = rows[ml0];
+          const bool whole = m + 15 < M && (r0.pos & 15) == 0 && rows[ml0 + 15].pos == r0.pos + 15;
+          const int hn = n - 2 * E.hidden, h = hn / E.head_dim, dd = hn - h * E.head_dim;
+          bf16_t* vt = (bf16_t*)E.vt + ((long)h * E.head_dim + dd) * E.T;
+          if (whole) {
+            // slot s of the group holds key vt_slot(s): swap the middle quads
+            float w[16];
+#pragma unroll
+            for (int q = 0; q < 16; ++q) w[q] = v[vt_slot(q)];
+            store16<bf16_t>(vt + r0.pos, w);
+          } else {
+#pragma unroll
+            for (int q = 0; q < 16; ++q)
+              if (m + q < M) vt[vt_slot(rows[ml0 + q].pos)] = f2bf(v[q]);
+          }
+        }
+        return;
+      }
       float v[16];
       static_for<4>([&](auto qq) {
         constexpr int q = decltype(qq)::value;
