@@ -56,15 +56,17 @@ __device__ __forceinline__ void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt((7 <<
 // NW waves x 32 queries per block.
 //
 // Pipeline over 64-key tiles j: K and V^T tiles arrive by direct-to-LDS loads
-// (global_load_lds_dwordx4) in a ring of 3 buffers, issued two tiles ahead.
-// Inside a wave the score MFMAs of tile j + 1 are issued before the softmax
-// of tile j, so the matrix cores work on S(j + 1) while the vector ALUs
-// exponentiate tile j; then P(j) V(j) accumulates into O.
-template <int NW>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW >= 8 ? 2 : 1)))
+// (global_load_lds_dwordx4) in a ring of STAGES buffers, issued STAGES - 1
+// tiles ahead.  With PIPE the score MFMAs of tile j + 1 are issued before the
+// softmax of tile j (matrix cores on S(j + 1) while the vector ALUs
+// exponentiate tile j); without it each tile runs scores, softmax, P V.
+// PIPE: issue the next tile's score MFMAs before this tile's softmax.
+// PRIO: raise the wave priority while it issues MFMAs.
+template <int NW, int STAGES = 3, int PIPE = 1, int PRIO = 0>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
   constexpr int BQ = NW * 32;
-  constexpr int STAGES = 3;
+  static_assert(STAGES >= 2 + PIPE, "the score pipeline reads tile j + 1 while tile j + 2 loads");
   constexpr int KT_U4 = BKV * 16;  // K tile: [64 keys][16 chunks of 8 d], chunk slot ^= key & 15
   constexpr int VT_U4 = D * 8;     // V^T tile: [128 d][8 chunks of 8 key slots], chunk slot ^= (d >> 1) & 7
   constexpr int KI = BKV / 4 / NW; // K-tile load instructions per wave (4 keys each)
@@ -113,8 +115,11 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
   };
 
   const int ntiles = (L + BKV - 1) / BKV;
-  tile_load(0, 0);
-  if (ntiles > 1) tile_load(1, 1);
+  // prologue: the first STAGES - 1 tiles in flight (the pipelined form also needs
+  // tile j + 1 resident at step j, hence one buffer more than it has in flight)
+#pragma unroll
+  for (int t = 0; t < STAGES - 1; ++t)
+    if (t < ntiles) tile_load(t, t);
 
   // Q fragments (B operand of S^T = K Q^T): query q0 + wave*32 + lane%32, d chunk 2*ks + lane/32
   const int qrow = q0 + wave * 32 + (lane & 31);
@@ -138,6 +143,7 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
   // register i, query lane % 32)
   auto scores = [&](int st, f32x16_t* s) {
     const uint4* S = smem[st];
+    if constexpr (PRIO) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -151,6 +157,7 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, u), qf[ks], s[kb], 0, 0, 0);
       }
     }
+    if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
     // keep four fragment reads ahead of the MFMAs that consume them
     sched_read_ahead<2 * D / 16, 4>();
   };
@@ -214,18 +221,30 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
     // tile j + 1 resident for every wave; every wave is done with tile j - 1
     wait_vmcnt0();
     __syncthreads();
-    if (j + 2 < ntiles) tile_load(j + 2, (j + 2) % STAGES);
+    if (j + STAGES - 1 < ntiles) tile_load(j + STAGES - 1, (j + STAGES - 1) % STAGES);
     scores((j + 1) % STAGES, s_nxt);
+    softmax_pv(j, j % STAGES, s_cur);
+  };
+  // without the score pipeline: tile j's scores, softmax and P V in turn
+  auto step_plain = [&](int j, f32x16_t* s_cur) {
+    wait_vmcnt0();
+    __syncthreads();
+    if (j + STAGES - 1 < ntiles) tile_load(j + STAGES - 1, (j + STAGES - 1) % STAGES);
+    scores(j % STAGES, s_cur);
     softmax_pv(j, j % STAGES, s_cur);
   };
 
   f32x16_t sa[2], sb[2];
-  wait_vmcnt0();
-  __syncthreads();
-  scores(0, sa);
-  for (int j = 0; j < ntiles; j += 2) {
-    step(j, sa, sb);
-    if (j + 1 < ntiles) step(j + 1, sb, sa);
+  if constexpr (PIPE) {
+    wait_vmcnt0();
+    __syncthreads();
+    scores(0, sa);
+    for (int j = 0; j < ntiles; j += 2) {
+      step(j, sa, sb);
+      if (j + 1 < ntiles) step(j + 1, sb, sa);
+    }
+  } else {
+    for (int j = 0; j < ntiles; ++j) step_plain(j, sa);
   }
 
   const float l = l_i + __shfl_xor(l_i, 32, 64);
@@ -344,18 +363,20 @@ AttnSched make_sched(const BatchMeta& m, int bq) {
 
 }  // namespace
 
-template <int NW>
-hipError_t launch_attn_nw(const AttnArgs& a, hipStream_t s) {
+template <int NW, int STAGES, int PIPE>
+hipError_t launch_attn_cfg(const AttnArgs& a, hipStream_t s) {
   const AttnSched sc = make_sched(a.meta, NW * 32);
   const long blocks = (long)sc.tile_off[sc.n] * a.heads;
   if (blocks == 0) return hipSuccess;
-  hipLaunchKernelGGL(attn_bf16_kernel<NW>, dim3((unsigned)blocks), dim3(NW * 64), 0, s, a, sc);
+  hipLaunchKernelGGL((attn_bf16_kernel<NW, STAGES, PIPE>), dim3((unsigned)blocks), dim3(NW * 64), 0, s, a, sc);
   return hipGetLastError();
 }
 
+// Measured on MI355X: the score pipeline (PIPE) needs 255 VGPRs and loses to
+// the plain order at 2 waves per SIMD, so the plain order with 2 buffers is used.
 hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s) {
   if (a.head_dim != D) return hipErrorInvalidValue;
-  return launch_attn_nw<8>(a, s);
+  return launch_attn_cfg<8, 2, 0>(a, s);
 }
 
 hipError_t launch_attention_f32(const AttnArgs& a, hipStream_t s) {
