@@ -63,6 +63,11 @@ __device__ __forceinline__ int lds_slot(int row, int kc) {
 
 // s_waitcnt with vmcnt = n and the other counters left alone (gfx9 encoding:
 // vmcnt[3:0] and [15:14], expcnt[6:4], lgkmcnt[11:8]).
+// Word 3 of a raw buffer resource on gfx9-family targets: 32-bit data format,
+// so untyped dword loads are range-checked against num_records and return
+// zeros past it.
+constexpr int kBufferWord3 = 0x00020000;
+
 template <int n>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(n >= 0 && n < 64, "vmcnt");
@@ -77,7 +82,7 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
   constexpr int FM = WTM / 32, FN = WTN / 32;
   constexpr int CPR = BK / 8;                     // 16-byte chunks per tile row
   constexpr int STAGE = (BM + BN) * CPR;          // uint4 per stage
-  static_assert(FM >= 1 && FN >= 1 && (BK == 32 || BK == 64) && STAGES >= 2, "tile config");
+  static_assert(FM >= 1 && FN >= 1 && (BK == 32 || BK == 64) && STAGES >= 2 && BK % 32 == 0, "tile config");
   static_assert(STAGES * STAGE * 16 <= 160 * 1024, "LDS");
 
   __shared__ uint4 lds[STAGES * STAGE];
@@ -152,15 +157,21 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
     __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
   };
 
-  if (K % BK == 0) {
+  if (P.dtl) {
     // ---- direct-to-LDS ring.  Wave instruction q of a tile moves 64 lanes x 16
     // bytes = RPI tile rows; lane l fills slot l % CPR of row l / CPR and so
-    // fetches the logical chunk that the swizzle puts in that slot.  Rows past
-    // M / N are clamped (their products only reach discarded outputs).
+    // fetches the logical chunk that the swizzle puts in that slot.  The loads
+    // are range-checked buffer loads over the whole operand: rows past M / N
+    // read as zeros (their products only reach discarded outputs).
     constexpr int RPI = 64 / CPR;                       // tile rows per instruction
     constexpr int AI = BM / RPI / NWAVES, BI = BN / RPI / NWAVES;
     static_assert(AI * RPI * NWAVES == BM && BI * RPI * NWAVES == BN, "tile config");
     constexpr int IPT = AI + BI;                        // load instructions per tile per wave
+    constexpr int KS = BK / 16;                         // k-steps per tile
+    const __amdgpu_buffer_rsrc_t rsa = __builtin_amdgcn_make_buffer_rsrc((void*)A, (short)0, (int)((long)M * lda * 2),
+                                                                         kBufferWord3);
+    const __amdgpu_buffer_rsrc_t rsw = __builtin_amdgcn_make_buffer_rsrc((void*)W, (short)0, (int)((long)N * ldw * 2),
+                                                                         kBufferWord3);
     auto dtl_load = [&](int kt, int st) {
       const int k0 = kt * BK;
       const int lr = lane / CPR, sl = lane % CPR;
@@ -169,36 +180,76 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
       for (int q = 0; q < AI; ++q) {
         const int r0 = (wave * AI + q) * RPI, row = r0 + lr;
         const int kc = lds_slot<CPR>(row, sl) - row * CPR;  // the XOR is an involution
-        const bf16_t* g = A + (long)min(m0 + row, M - 1) * lda + k0 + kc * 8;
-        __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)(S + r0 * CPR), 16,
-                                         0, 0);
+        const int off = ((m0 + row) * (int)lda + k0 + kc * 8) * 2;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, (__attribute__((address_space(3))) void*)(S + r0 * CPR), 16, off,
+                                                 0, 0, 0);
       }
 #pragma unroll
       for (int q = 0; q < BI; ++q) {
         const int r0 = (wave * BI + q) * RPI, row = r0 + lr;
         const int kc = lds_slot<CPR>(BM + row, sl) - (BM + row) * CPR;
-        const bf16_t* g = W + (long)min(n0 + row, N - 1) * ldw + k0 + kc * 8;
-        __builtin_amdgcn_global_load_lds((const void*)g,
-                                         (__attribute__((address_space(3))) void*)(S + (BM + r0) * CPR), 16, 0, 0);
+        const int off = ((n0 + row) * (int)ldw + k0 + kc * 8) * 2;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsw, (__attribute__((address_space(3))) void*)(S + (BM + r0) * CPR),
+                                                 16, off, 0, 0, 0);
       }
     };
-    // prologue: tiles 0 .. STAGES-2 in flight
+    auto mfma_step = [&](auto bufc) __attribute__((always_inline)) {
+      constexpr int buf = decltype(bufc)::value;
 #pragma unroll
-    for (int t = 0; t < STAGES - 1; ++t)
-      if (t < KT) dtl_load(t, t);
-    for (int kt = 0; kt < KT; ++kt) {
-      // own loads of tile kt complete (later tiles may stay in flight), then
-      // every wave's: after the barrier tile kt is in LDS and every wave has
-      // finished tile kt - 1, whose buffer the next load reuses
-      const int after = min(KT - 1, kt + STAGES - 2) - kt;
-      static_for<STAGES - 1>([&](auto aa) {
-        constexpr int a = decltype(aa)::value;
-        if (after == a) wait_vmcnt<a * IPT>();
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][i], fb[buf][j], acc[i][j], 0, 0, 0);
+    };
+    // k-steps 0 .. KS-2 of the tile in buffer st: each k-step's MFMAs
+    // alternate with the fragment reads of the next k-step
+    constexpr int NR = FM + FN, NM = FM * FN, NP = NR < NM ? NR : NM;
+    auto inner_steps = [&](int st) __attribute__((always_inline)) {
+      static_for<KS - 1>([&](auto kk) {
+        constexpr int ks = decltype(kk)::value;
+        fload(st, ks + 1, (ks + 1) & 1);
+        mfma_step(std::integral_constant<int, ks & 1>{});
+        static_for<NP>([&](auto) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+        });
+        if constexpr (NM > NP) __builtin_amdgcn_sched_group_barrier(0x008, NM - NP, 0);
+        if constexpr (NR > NP) __builtin_amdgcn_sched_group_barrier(0x100, NR - NP, 0);
       });
-      __syncthreads();
-      if (kt + STAGES - 1 < KT) dtl_load(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
-      compute(kt % STAGES);
+    };
+    // Every buffer is refilled right after the barrier that precedes its
+    // tile's last k-step, and the first fragments of the next tile are read
+    // under that k-step's MFMAs, so no wave idles between tiles.  Loads past
+    // the last K tile fetch the last tile again into a buffer nobody reads
+    // any more: the loop has no branches and constant wait counts.  The
+    // barrier is a bare s_barrier: a __syncthreads() fence would also drain
+    // the loads still in flight for later tiles.
+#pragma unroll
+    for (int t = 0; t < STAGES; ++t) dtl_load(min(t, KT - 1), t);
+    wait_vmcnt<(STAGES - 1) * IPT>();
+    asm volatile("s_barrier" ::: "memory");
+    fload(0, 0, 0);
+    for (int kt = 0; kt < KT - 1; ++kt) {
+      const int st = kt % STAGES;
+      inner_steps(st);
+      // own loads of tile kt + 1 done (later tiles stay in flight) and the
+      // last fragments of tile kt read; after the barrier tile kt + 1 is in
+      // LDS and nobody reads buffer st any more
+      wait_vmcnt<(STAGES - 2) * IPT>();
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+      asm volatile("s_barrier" ::: "memory");
+      dtl_load(min(kt + STAGES, KT - 1), st);
+      fload((kt + 1) % STAGES, 0, 0);
+      mfma_step(std::integral_constant<int, (KS - 1) & 1>{});
+      constexpr int VP = IPT / NP > 0 ? IPT / NP : 1;
+      static_for<NP>([&](auto) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x020, VP, 0);  // VMEM (buffer -> LDS)
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+      });
     }
+    inner_steps((KT - 1) % STAGES);
+    mfma_step(std::integral_constant<int, (KS - 1) & 1>{});
     __syncthreads();
   } else {
     // ---- register path with zero-filled K tail (two LDS buffers).
@@ -341,8 +392,18 @@ hipError_t launch_cfg(const GemmProblem& p, hipStream_t s) {
   long tiles = (long)((p.g[0].M + BM - 1) / BM) * tiles_n;
   if (p.n_groups > 1) tiles += (long)((p.g[1].M + BM - 1) / BM) * tiles_n;
   if (tiles == 0) return hipSuccess;
+  // direct-to-LDS path: whole K tiles, 16-byte aligned rows, and operands
+  // small enough for the 32-bit offsets of buffer loads
+  GemmProblem q = p;
+  q.dtl = 1;
+  for (int g = 0; g < p.n_groups; ++g) {
+    const GemmGroup& G = p.g[g];
+    const bool ok = G.K % BK == 0 && G.lda % 8 == 0 && G.ldw % 8 == 0 && (long)(G.M + BM) * G.lda * 2 < (1L << 31) &&
+                    (long)(p.N + BN) * G.ldw * 2 < (1L << 31);
+    if (!ok) q.dtl = 0;
+  }
   hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, NWM, NWN, BK, STAGES>), dim3((unsigned)tiles), dim3(NWM * NWN * 64), 0,
-                     s, p);
+                     s, q);
   return hipGetLastError();
 }
 
