@@ -40,14 +40,17 @@ __global__ void timestep_kernel(float* e, int n_req, TimeArgs ta, int dim) {
 // ---------------------------------------------------------------- GEMV
 // y[r, o] = sum_k W[o, k] act(x[r, k]) + b[o] for up to 4 requests per pass;
 // one wavefront per output row, activations staged in LDS, weights streamed
-// once with 16-byte loads.
+// once with 16-byte loads.  The stream is latency-bound unless many loads are
+// in flight: a lane requests all its chunks of a row at once (up to GV_C), and
+// the next row's before it reduces the current one.
 constexpr int GV_R = 4;
+constexpr int GV_C = 8;  // prefetched 16-byte chunks per lane and row
 
 template <typename WT>
 __global__ __launch_bounds__(256) void gemv_kernel(const WT* __restrict__ W, const WT* __restrict__ b,
                                                    const float* __restrict__ x, long ldx, int n_req, int K,
                                                    int N, int act, float* __restrict__ y, long ldy) {
-  extern __shared__ float xs[];  // [GV_R][K]
+  extern __shared__ float xs[];  // [n_req][K]
   const int nr = min(n_req, GV_R);
   for (int i = threadIdx.x; i < nr * K; i += blockDim.x) {
     const int r = i / K, k = i % K;
@@ -60,51 +63,76 @@ __global__ __launch_bounds__(256) void gemv_kernel(const WT* __restrict__ W, con
   const int wave = threadIdx.x >> 6;
   const int nwaves = (gridDim.x * blockDim.x) >> 6;
   const int chunks = K / EPC;
-  for (int o = blockIdx.x * 4 + wave; o < N; o += nwaves) {
-    float acc[GV_R] = {0.f, 0.f, 0.f, 0.f};
-    const WT* wr = W + (long)o * K;
-    for (int c = lane; c < chunks; c += 64) {
-      const uint4 u = *(const uint4*)(wr + c * EPC);
-      float wv[EPC];
-      if constexpr (sizeof(WT) == 2) {
-        const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+  auto fetch = [&](int o, uint4* u) {
+    const WT* wr = W + (long)min(o, N - 1) * K;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          wv[2 * e] = __uint_as_float(w4[e] << 16);
-          wv[2 * e + 1] = __uint_as_float(w4[e] & 0xFFFF0000u);
-        }
-      } else {
-        wv[0] = __uint_as_float(u.x);
-        wv[1] = __uint_as_float(u.y);
-        wv[2] = __uint_as_float(u.z);
-        wv[3] = __uint_as_float(u.w);
+    for (int i = 0; i < GV_C; ++i) {
+      const int c = lane + 64 * i;
+      if (c < chunks) u[i] = *(const uint4*)(wr + c * EPC);
+    }
+  };
+  auto dot = [&](const uint4& u, int c, float* acc) {
+    float wv[EPC];
+    if constexpr (sizeof(WT) == 2) {
+      const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        wv[2 * e] = __uint_as_float(w4[e] << 16);
+        wv[2 * e + 1] = __uint_as_float(w4[e] & 0xFFFF0000u);
       }
-#pragma unroll
-      for (int r = 0; r < GV_R; ++r) {
-        if (r < nr) {
-          const float* xr = xs + r * K + c * EPC;
-#pragma unroll
-          for (int e = 0; e < EPC; ++e) acc[r] = fmaf(wv[e], xr[e], acc[r]);
-        }
-      }
+    } else {
+      wv[0] = __uint_as_float(u.x);
+      wv[1] = __uint_as_float(u.y);
+      wv[2] = __uint_as_float(u.z);
+      wv[3] = __uint_as_float(u.w);
     }
 #pragma unroll
     for (int r = 0; r < GV_R; ++r) {
       if (r < nr) {
-        const float s = wave_sum(acc[r]);
-        if (lane == 0) y[(long)r * ldy + o] = s + (b ? to_f32<WT>(b[o]) : 0.f);
+        const float* xr = xs + r * K + c * EPC;
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) acc[r] = fmaf(wv[e], xr[e], acc[r]);
       }
     }
+  };
+  // row o from the prefetched chunks u (plus any chunks past the prefetch window)
+  auto row = [&](int o, const uint4* u) {
+    float acc[GV_R] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < GV_C; ++i) {
+      const int c = lane + 64 * i;
+      if (c < chunks) dot(u[i], c, acc);
+    }
+    for (int c = lane + 64 * GV_C; c < chunks; c += 64) dot(*(const uint4*)(W + (long)o * K + c * EPC), c, acc);
+#pragma unroll
+    for (int r = 0; r < GV_R; ++r) {
+      if (r < nr) {
+        const float sum = wave_sum(acc[r]);
+        if (lane == 0) y[(long)r * ldy + o] = sum + (b ? to_f32<WT>(b[o]) : 0.f);
+      }
+    }
+  };
+  uint4 ua[GV_C], ub[GV_C];
+  int o = blockIdx.x * 4 + wave;
+  if (o < N) fetch(o, ua);
+  for (; o < N; o += 2 * nwaves) {
+    if (o + nwaves < N) fetch(o + nwaves, ub);
+    row(o, ua);
+    if (o + nwaves >= N) break;
+    if (o + 2 * nwaves < N) fetch(o + 2 * nwaves, ua);
+    row(o + nwaves, ub);
   }
 }
 
 // ---------------------------------------------------------------- adaLN LayerNorm
 // out = LN(x) * (1 + scale[req]) + shift[req], LN with biased variance and no
 // affine; statistics in fp32 with a two-pass (mean, then centred squares)
-// evaluation from registers.  One wavefront per row; H <= 64 * 4 * 16.
-constexpr int LN_MAXV = 16;  // float4 per lane
+// evaluation from registers.  One wavefront per row, NV float4 per lane
+// (H <= 256 NV, at most LN_MAX_H), NV fixed at compile time so the row uses
+// no more registers than it needs and more rows stay in flight.
+constexpr int LN_MAX_H = 4096;
 
-template <typename OT>
+template <typename OT, int NV>
 __global__ __launch_bounds__(256) void ln_mod_kernel(const float* __restrict__ X, int H, int row_begin,
                                                      int row_end, const BatchMeta meta,
                                                      const float* __restrict__ mods, int mods_ld, int sh_t,
@@ -115,22 +143,27 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const float* __restrict__ X
   if (R >= row_end) return;
   const int H4 = H >> 2;
   const float4* xr = (const float4*)(X + (long)R * H);
-  float4 v[LN_MAXV];
-  float s = 0.f;
+  const RowInfo ri = row_info(meta, R);
+  const float* mrow = mods + (long)ri.req * mods_ld;
+  const float4* shv = (const float4*)(mrow + (ri.is_img ? sh_i : sh_t));
+  const float4* scv = (const float4*)(mrow + (ri.is_img ? sc_i : sc_t));
+  float4 v[NV];
 #pragma unroll
-  for (int i = 0; i < LN_MAXV; ++i) {
+  for (int i = 0; i < NV; ++i) {
     const int c = lane + i * 64;
     if (c < H4) {
       v[i] = xr[c];
-      s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
     }
   }
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i)
+    if (lane + i * 64 < H4) s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
   const float mean = wave_sum(s) / (float)H;
   float ss = 0.f;
 #pragma unroll
-  for (int i = 0; i < LN_MAXV; ++i) {
-    const int c = lane + i * 64;
-    if (c < H4) {
+  for (int i = 0; i < NV; ++i) {
+    if (lane + i * 64 < H4) {
       v[i].x -= mean;
       v[i].y -= mean;
       v[i].z -= mean;
@@ -139,13 +172,9 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const float* __restrict__ X
     }
   }
   const float rstd = 1.0f / sqrtf(wave_sum(ss) / (float)H + eps);
-  const RowInfo ri = row_info(meta, R);
-  const float* mrow = mods + (long)ri.req * mods_ld;
-  const float4* shv = (const float4*)(mrow + (ri.is_img ? sh_i : sh_t));
-  const float4* scv = (const float4*)(mrow + (ri.is_img ? sc_i : sc_t));
   OT* orow = out + (long)(R - row_begin) * ldo;
 #pragma unroll
-  for (int i = 0; i < LN_MAXV; ++i) {
+  for (int i = 0; i < NV; ++i) {
     const int c = lane + i * 64;
     if (c < H4) {
       const float4 sh = shv[c], sc = scv[c];
@@ -246,7 +275,7 @@ hipError_t launch_timestep_embed(float* e, int n_req, const float* t_host, int d
 
 hipError_t launch_gemv(int wdtype, const void* W, const void* b, const float* x, long ldx, int n_req, int K,
                        int N, int act, float* y, long ldy, hipStream_t s) {
-  const size_t shmem = (size_t)GV_R * K * sizeof(float);
+  const size_t shmem = (size_t)(n_req < GV_R ? n_req : GV_R) * K * sizeof(float);
   int blocks = (N + 3) / 4;
   if (blocks > 256 * 16) blocks = 256 * 16;
   for (int r0 = 0; r0 < n_req; r0 += GV_R) {
@@ -268,13 +297,25 @@ hipError_t launch_ln_modulate(int out_dtype, const float* X, int H, int row_begi
                               int shift_img, int scale_img, float eps, void* out, long ldo, hipStream_t s) {
   const int rows = row_end - row_begin;
   if (rows <= 0) return hipSuccess;
+  if (H > LN_MAX_H) return hipErrorInvalidValue;
   const dim3 grid((rows + 3) / 4);
-  if (out_dtype == DIT_BF16)
-    hipLaunchKernelGGL(ln_mod_kernel<bf16_t>, grid, dim3(256), 0, s, X, H, row_begin, row_end, meta, mods, mods_ld,
-                       shift_txt, scale_txt, shift_img, scale_img, eps, (bf16_t*)out, ldo);
-  else
-    hipLaunchKernelGGL(ln_mod_kernel<float>, grid, dim3(256), 0, s, X, H, row_begin, row_end, meta, mods, mods_ld,
-                       shift_txt, scale_txt, shift_img, scale_img, eps, (float*)out, ldo);
+  const int nv = (H / 4 + 63) / 64;
+#define DIT_LN_LAUNCH(OT, NV)                                                                                 \
+  hipLaunchKernelGGL((ln_mod_kernel<OT, NV>), grid, dim3(256), 0, s, X, H, row_begin, row_end, meta, mods, mods_ld, \
+                     shift_txt, scale_txt, shift_img, scale_img, eps, (OT*)out, ldo)
+#define DIT_LN_DISPATCH(OT)          \
+  if (nv <= 2) DIT_LN_LAUNCH(OT, 2);  \
+  else if (nv <= 4) DIT_LN_LAUNCH(OT, 4); \
+  else if (nv <= 8) DIT_LN_LAUNCH(OT, 8); \
+  else if (nv <= 12) DIT_LN_LAUNCH(OT, 12); \
+  else DIT_LN_LAUNCH(OT, 16);
+  if (out_dtype == DIT_BF16) {
+    DIT_LN_DISPATCH(bf16_t)
+  } else {
+    DIT_LN_DISPATCH(float)
+  }
+#undef DIT_LN_DISPATCH
+#undef DIT_LN_LAUNCH
   return hipGetLastError();
 }
 
