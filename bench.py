@@ -203,6 +203,43 @@ def run_sp_share(torch, dit, synth, workloads, wl, cfg, w, steps, seed, dev):
                     f"launches of {heads} heads over {L} tokens (HIP events); all-to-alls excluded"}
 
 
+def scheduler_latency(seed: int):
+    """Decision latency of the round scheduler (host C++): one ts_round_schedule
+    call over R pending requests of the paper's resolution mix on N = 8 GPUs,
+    their allocations from ts_allocate with the MI355X cost model, timed
+    around the C call alone (arguments marshalled once)."""
+    import ctypes
+    import random
+    from paper_2510_01565_amd import cost_model, sched
+    rng = random.Random(seed)
+    out = {}
+    for n_req in (16, 64, 256):
+        reqs = []
+        for _ in range(n_req):
+            res = rng.choice([256, 512, 1024, 2048])
+            row = cost_model.row(res)
+            steps = rng.randint(1, 28)
+            deadline = rng.randint(steps * row[0] // 4, steps * row[0] * 2)
+            _, alloc, _, _ = sched.allocate(row, 8, steps, deadline)
+            reqs.append(sched.Request(deadline, row, alloc))
+        arr = sched._requests(reqs)
+        dec = (sched.ts_decision * n_req)()
+        sv, used = ctypes.c_int32(), ctypes.c_int32()
+        L = sched.lib()
+        tau = 5 * cost_model.step_us(1024, 1)
+        reps = 200
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            L.ts_round_schedule(arr, n_req, 8, tau, 0, dec, ctypes.byref(sv), ctypes.byref(used))
+        out[str(n_req)] = round((time.perf_counter() - t0) / reps * 1e6, 2)
+    row = cost_model.row(2048)
+    t0 = time.perf_counter()
+    for _ in range(200):
+        sched.allocate(row, 8, 28, 28 * row[0] // 3)
+    return {"round_schedule_us_by_requests": out, "n_gpus": 8,
+            "allocate_us_28_steps": round((time.perf_counter() - t0) / 200 * 1e6, 2)}
+
+
 def roofline(kernels, dtype: str, workload: str):
     """Dominant kernel family by time: algorithmic work per launch over its
     average launch duration (HIP events on the launch stream)."""
@@ -330,6 +367,12 @@ def main() -> int:
         log("timing the CPU oracle on a bounded sample")
         cpu = cpu_baseline(wl, args.seed)
         log(f"cpu baseline: {cpu['sample']}")
+    sched_lat = None
+    try:
+        sched_lat = scheduler_latency(args.seed)
+        log(f"scheduler decision latency (us) by pending requests: {sched_lat['round_schedule_us_by_requests']}")
+    except (OSError, RuntimeError) as e:  # scheduler library not built
+        log(f"scheduler latency not measured: {e}")
     g = wl.grids()
     out = {
         "metric": METRIC, "value": main_res["steps_per_s"], "unit": "steps/s", "n_gpus": 1, "steps": args.steps,
@@ -339,7 +382,7 @@ def main() -> int:
                    "text_tokens": wl.n_txt, "requests": len(g), "parallelism": "single GPU"},
         "tflops": main_res["tflops"], "frac_bf16_peak": main_res["frac_peak"],
         "tflop_per_step": main_res["tflop_per_step"], "cv_pct": main_res["cv_pct"],
-        "roofline": rl, "cpu_baseline": cpu, "per_workload": per,
+        "roofline": rl, "cpu_baseline": cpu, "per_workload": per, "scheduler": sched_lat,
         "kernels_ms_per_step": {k: round(v["ms_per_step"], 4) for k, v in main_res["kernels"].items()
                                 if not k.startswith("detail:")},
         "kernels": {k: {"launches_per_step": v["launches"] // max(1, min(args.steps, 3)), "avg_launch_ms": v["ms"] / v["launches"],

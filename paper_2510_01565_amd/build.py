@@ -1,8 +1,12 @@
-"""Builds the HIP library ``libdit_mi355x.so`` in-tree for gfx950.
+"""Builds the libraries in-tree.
 
-Every ``csrc/*.hip`` file is compiled by hipcc to an object (in parallel) and
-linked into one shared library next to this file.  Run as
-``python -m paper_2510_01565_amd.build`` or through ``__graft_entry__.build()``.
+* ``libdit_mi355x.so``: every ``csrc/*.hip`` file compiled by hipcc for
+  gfx950 (in parallel) and linked into one shared library;
+* ``libtetri_sched.so``: the host-only round scheduler (``csrc/host/*.cpp``),
+  compiled by the host C++ compiler.
+
+Run as ``python -m paper_2510_01565_amd.build`` or through
+``__graft_entry__.build()``.
 """
 from __future__ import annotations
 
@@ -17,6 +21,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libdit_mi355x.so")
+SCHED_LIB = os.path.join(HERE, "libtetri_sched.so")
+CXX = shutil.which("g++") or shutil.which("c++") or "g++"
 ARCH = "gfx950"
 
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
@@ -50,7 +56,21 @@ def build(verbose: bool = True) -> str:
     os.replace(tmp, LIB)
     if verbose:
         print(f"built {LIB} from {len(srcs)} sources", file=sys.stderr)
+    build_sched(verbose)
     return LIB
+
+
+def build_sched(verbose: bool = True) -> str:
+    srcs = sorted(glob.glob(os.path.join(CSRC, "host", "*.cpp")))
+    tmp = SCHED_LIB + ".tmp"
+    cmd = [CXX, "-O2", "-std=c++17", "-fPIC", "-shared", "-Wall", "-o", tmp, *srcs]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"scheduler build failed:\n{r.stdout}\n{r.stderr}")
+    os.replace(tmp, SCHED_LIB)
+    if verbose:
+        print(f"built {SCHED_LIB} from {len(srcs)} sources", file=sys.stderr)
+    return SCHED_LIB
 
 
 if __name__ == "__main__":

@@ -72,10 +72,42 @@ WORKLOADS = {
         "dit57_2048px_sp4_share_bf16", FLUX_FULL, [2048], [512], t=[0.5], kind="attention_share",
         note="one GPU's share of a 4-way sequence-parallel split: 6 of 24 heads over 16896 tokens",
         extra={"sp": 4}),
+    "dit57_256px_bf16": Workload(
+        "dit57_256px_bf16", FLUX_FULL, [256], [512], t=[0.5],
+        note="19 double + 38 single blocks, 512 text + 256 image tokens, bf16 (cost-model row)"),
+    "dit57_512px_bf16": Workload(
+        "dit57_512px_bf16", FLUX_FULL, [512], [512], t=[0.5],
+        note="19 double + 38 single blocks, 512 text + 1024 image tokens, bf16 (cost-model row)"),
+    # selective continuous batching (section 3, section 5): B identical small-resolution
+    # requests stepped together, each at its own timestep
+    "dit57_256px_x4_bf16": Workload(
+        "dit57_256px_x4_bf16", FLUX_FULL, [256] * 4, [512] * 4, t=None,
+        note="4 identical 256 px requests batched in one step"),
+    "dit57_256px_x8_bf16": Workload(
+        "dit57_256px_x8_bf16", FLUX_FULL, [256] * 8, [512] * 8, t=None,
+        note="8 identical 256 px requests batched in one step"),
+    "dit57_512px_x2_bf16": Workload(
+        "dit57_512px_x2_bf16", FLUX_FULL, [512] * 2, [512] * 2, t=None,
+        note="2 identical 512 px requests batched in one step"),
+    "dit57_512px_x4_bf16": Workload(
+        "dit57_512px_x4_bf16", FLUX_FULL, [512] * 4, [512] * 4, t=None,
+        note="4 identical 512 px requests batched in one step"),
     "dit57_packed_mixed_bf16": Workload(
         "dit57_packed_mixed_bf16", FLUX_FULL, [256, 512, 1024, 2048], [512, 512, 512, 512], t=None,
         note="4 requests 256/512/1024/2048 px packed, per-request timesteps U[0,1)"),
 }
+
+# One GPU's share of a k-way sequence-parallel step at every resolution of the
+# paper's workload mix (256 .. 2048 px, section 6.1): the per-GPU compute of
+# the cost model's T(k) rows.
+for _res in (256, 512, 1024, 2048):
+    for _k in (2, 4, 8):
+        _name = f"dit57_{_res}px_sp{_k}_share_bf16"
+        if _name not in WORKLOADS:
+            WORKLOADS[_name] = Workload(
+                _name, FLUX_FULL, [_res], [512], t=[0.5], kind="attention_share",
+                note=f"one GPU's share of a {_k}-way sequence-parallel split at {_res} px",
+                extra={"sp": _k})
 
 
 def flops_per_step(m: ModelShape, n_txt: List[int], n_img: List[int]) -> dict:
