@@ -122,7 +122,6 @@ struct GemmGroup {
 struct GemmProblem {
   int N;
   int n_groups;  // 1 or 2
-  int dtl;       // set by the launcher: operands fit the direct-to-LDS path
   GemmGroup g[2];
   BatchMeta meta;
 };

@@ -22,6 +22,11 @@ namespace dit {
 
 namespace {
 
+// k-steps over which the loads of one K tile are spread (direct-to-LDS path)
+constexpr int kLoadSplitK = 1;
+// main-loop schedule of the direct-to-LDS path (0: one barrier per K tile, 1: whole-tile register prefetch)
+constexpr int kSchedK = 1;
+
 struct TileCoord {
   int group, m0, n0;
 };
@@ -74,7 +79,7 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-template <int BM, int BN, int NWM, int NWN, int BK, int STAGES>
+template <int BM, int BN, int NWM, int NWN, int BK, int STAGES, bool DTL>
 __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProblem P) {
   constexpr int NT = NWM * NWN * 64;
   constexpr int NWAVES = NWM * NWN;
@@ -157,41 +162,97 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
     __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
   };
 
-  if (P.dtl) {
-    // ---- direct-to-LDS ring.  Wave instruction q of a tile moves 64 lanes x 16
-    // bytes = RPI tile rows; lane l fills slot l % CPR of row l / CPR and so
-    // fetches the logical chunk that the swizzle puts in that slot.  The loads
-    // are range-checked buffer loads over the whole operand: rows past M / N
-    // read as zeros (their products only reach discarded outputs).
+  if (DTL) {  // a compile-time constant: the other path is dropped
+    // ---- direct-to-LDS ring.  LDS holds [A stage 0 .. STAGES-1 | B stage 0 ..
+    // STAGES-1], rows of BK bf16 (CPR 16-byte chunks, XOR-swizzled).  Wave
+    // instruction q of a tile moves 64 lanes x 16 bytes = RPI tile rows; lane l
+    // fills slot l % CPR of row l / CPR and so fetches the logical chunk that
+    // the swizzle puts in that slot.  Loads are range-checked buffer loads
+    // over the whole operand: rows past M / N read as zeros (their products
+    // only reach discarded outputs).
+    //
+    // Every address is fixed before the loop: a lane's global offset of each
+    // load instruction (the k offset of a tile travels in the scalar offset),
+    // the LDS destination of each instruction (scalar, wave-uniform) and the
+    // lane's LDS fragment address for each k-step (the stage and fragment
+    // index are immediate offsets), so the loop issues MFMAs, LDS reads and
+    // buffer loads and almost no vector ALU work.
     constexpr int RPI = 64 / CPR;                       // tile rows per instruction
     constexpr int AI = BM / RPI / NWAVES, BI = BN / RPI / NWAVES;
     static_assert(AI * RPI * NWAVES == BM && BI * RPI * NWAVES == BN, "tile config");
     constexpr int IPT = AI + BI;                        // load instructions per tile per wave
     constexpr int KS = BK / 16;                         // k-steps per tile
+    constexpr int ROWB = CPR * 16;                      // bytes per LDS row
+    constexpr int A_STAGE = BM * ROWB, B_STAGE = BN * ROWB;
+    constexpr int B_REGION = STAGES * A_STAGE;
+    static_assert(B_REGION + STAGES * B_STAGE <= (int)sizeof(lds), "LDS");
+    static_assert((STAGES - 1) * A_STAGE + (FM - 1) * 32 * ROWB < 65536 &&
+                  (STAGES - 1) * B_STAGE + (FN - 1) * 32 * ROWB < 65536, "ds_read immediate offsets");
+    const int wv = __builtin_amdgcn_readfirstlane(wave);  // wave index in a scalar register
     const __amdgpu_buffer_rsrc_t rsa = __builtin_amdgcn_make_buffer_rsrc((void*)A, (short)0, (int)((long)M * lda * 2),
                                                                          kBufferWord3);
     const __amdgpu_buffer_rsrc_t rsw = __builtin_amdgcn_make_buffer_rsrc((void*)W, (short)0, (int)((long)N * ldw * 2),
                                                                          kBufferWord3);
-    auto dtl_load = [&](int kt, int st) {
-      const int k0 = kt * BK;
+    // per-lane global byte offsets of the load instructions (k offset excluded)
+    int goa[AI], gob[BI];
+    {
       const int lr = lane / CPR, sl = lane % CPR;
-      uint4* S = lds + st * STAGE;
 #pragma unroll
       for (int q = 0; q < AI; ++q) {
-        const int r0 = (wave * AI + q) * RPI, row = r0 + lr;
+        const int row = (wv * AI + q) * RPI + lr;
         const int kc = lds_slot<CPR>(row, sl) - row * CPR;  // the XOR is an involution
-        const int off = ((m0 + row) * (int)lda + k0 + kc * 8) * 2;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, (__attribute__((address_space(3))) void*)(S + r0 * CPR), 16, off,
-                                                 0, 0, 0);
+        goa[q] = ((m0 + row) * (int)lda + kc * 8) * 2;
       }
 #pragma unroll
       for (int q = 0; q < BI; ++q) {
-        const int r0 = (wave * BI + q) * RPI, row = r0 + lr;
-        const int kc = lds_slot<CPR>(BM + row, sl) - (BM + row) * CPR;
-        const int off = ((n0 + row) * (int)ldw + k0 + kc * 8) * 2;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsw, (__attribute__((address_space(3))) void*)(S + (BM + r0) * CPR),
-                                                 16, off, 0, 0, 0);
+        const int row = (wv * BI + q) * RPI + lr;
+        const int kc = lds_slot<CPR>(row, sl) - row * CPR;
+        gob[q] = ((n0 + row) * (int)ldw + kc * 8) * 2;
       }
+    }
+    // per-lane LDS byte address of fragment 0 at k-step ks, stage 0.  Rows of
+    // fragment i differ by 32 i, which leaves the swizzle term unchanged.
+    int fra[KS], frb[KS];
+    {
+      const int ra = wm * WTM + (lane & 31), rb = wn * WTN + (lane & 31);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        fra[ks] = lds_slot<CPR>(ra, 2 * ks + (lane >> 5)) * 16;
+        frb[ks] = B_REGION + lds_slot<CPR>(rb, 2 * ks + (lane >> 5)) * 16;
+      }
+    }
+    char* const lbase = (char*)lds;
+    // load instructions [q0, q1) of tile kt (A's first, then B's) into stage st
+    auto load_part = [&](int st, int kt, int q0, int q1) __attribute__((always_inline)) {
+      const int koff = kt * BK * 2;
+#pragma unroll
+      for (int q = 0; q < AI; ++q) {
+        if (q < q0 || q >= q1) continue;
+        // copied to a local first: the array element passed straight to the
+        // builtin makes the host pass drop the kernel launch stub
+        const int vo = goa[q];
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rsa, (__attribute__((address_space(3))) void*)(lbase + st * A_STAGE + (wv * AI + q) * RPI * ROWB), 16,
+            vo, koff, 0, 0);
+      }
+#pragma unroll
+      for (int q = 0; q < BI; ++q) {
+        if (AI + q < q0 || AI + q >= q1) continue;
+        const int vo = gob[q];
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rsw,
+            (__attribute__((address_space(3))) void*)(lbase + B_REGION + st * B_STAGE + (wv * BI + q) * RPI * ROWB),
+            16, vo, koff, 0, 0);
+      }
+    };
+    auto read_frags = [&](auto stc, auto ksc, auto bufc) __attribute__((always_inline)) {
+      constexpr int st = decltype(stc)::value, ks = decltype(ksc)::value, buf = decltype(bufc)::value;
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        fa[buf][i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(lbase + fra[ks] + st * A_STAGE + i * 32 * ROWB));
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        fb[buf][j] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(lbase + frb[ks] + st * B_STAGE + j * 32 * ROWB));
     };
     auto mfma_step = [&](auto bufc) __attribute__((always_inline)) {
       constexpr int buf = decltype(bufc)::value;
@@ -201,55 +262,157 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
         for (int j = 0; j < FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][i], fb[buf][j], acc[i][j], 0, 0, 0);
     };
-    // k-steps 0 .. KS-2 of the tile in buffer st: each k-step's MFMAs
-    // alternate with the fragment reads of the next k-step
     constexpr int NR = FM + FN, NM = FM * FN, NP = NR < NM ? NR : NM;
-    auto inner_steps = [&](int st) __attribute__((always_inline)) {
+    using I0 = std::integral_constant<int, 0>;
+    if constexpr (kSchedK == 1) {
+    // ---- whole-tile register prefetch, two barriers per K tile.
+    // Fragment registers hold one whole K tile (one buffer per k-step).  The
+    // fragments of tile X are read during the last k-step of tile X-1 (k-steps
+    // 0, 1) and the first k-step of X (k-steps 2, 3); after a barrier at the
+    // start of X's second k-step nobody reads X's stage any more and the loads
+    // of tile X+2 into it are issued over X's k-steps 1 and 2 (about the rate
+    // the texture path drains them); a second barrier before X's last k-step
+    // makes tile X+1 visible.  A load thus has about one K tile between its
+    // issue and the barrier that needs it.
+    static_assert(KS == 4 && STAGES == 2, "schedule for 64-wide K tiles");
+    bf16x8_t ga[KS][FM], gb[KS][FN];
+    auto rd = [&](auto stc, auto ksc) __attribute__((always_inline)) {
+      constexpr int st = decltype(stc)::value, ks = decltype(ksc)::value;
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        ga[ks][i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(lbase + fra[ks] + st * A_STAGE + i * 32 * ROWB));
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        gb[ks][j] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(lbase + frb[ks] + st * B_STAGE + j * 32 * ROWB));
+    };
+    auto mm = [&](auto ksc) __attribute__((always_inline)) {
+      constexpr int ks = decltype(ksc)::value;
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga[ks][i], gb[ks][j], acc[i][j], 0, 0, 0);
+    };
+    // interleave: NM MFMAs with R DS reads and V VMEM loads spread evenly
+    auto weave = [&](auto rc, auto vc) __attribute__((always_inline)) {
+      constexpr int R = decltype(rc)::value, V = decltype(vc)::value;
+      static_for<NM>([&](auto mc) {
+        constexpr int m = decltype(mc)::value;
+        constexpr int r = (m + 1) * R / NM - m * R / NM, v = (m + 1) * V / NM - m * V / NM;
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);
+        if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x020, v, 0);
+      });
+    };
+    constexpr int HALF = IPT / 2;
+    using K0 = std::integral_constant<int, 0>;
+    using K1 = std::integral_constant<int, 1>;
+    using K2 = std::integral_constant<int, 2>;
+    using K3 = std::integral_constant<int, 3>;
+    auto tile2 = [&](auto stc, int kt) __attribute__((always_inline)) {
+      constexpr int st = decltype(stc)::value;
+      using SN = std::integral_constant<int, st ^ 1>;
+      // k-step 0: read this tile's k-steps 2, 3
+      rd(stc, K2{});
+      rd(stc, K3{});
+      mm(K0{});
+      weave(std::integral_constant<int, 2 * NR>{}, K0{});
+      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): own reads of this stage done
+      asm volatile("s_barrier" ::: "memory");
+      // k-steps 1, 2: loads of tile kt + 2 into this stage
+      load_part(st, min(kt + 2, KT - 1), 0, HALF);
+      mm(K1{});
+      weave(K0{}, std::integral_constant<int, HALF>{});
+      __builtin_amdgcn_sched_barrier(0);
+      load_part(st, min(kt + 2, KT - 1), HALF, IPT);
+      mm(K2{});
+      weave(K0{}, std::integral_constant<int, IPT - HALF>{});
+      __builtin_amdgcn_sched_barrier(0);
+      // tile kt + 1 landed (only the loads of kt + 2 may still be in flight)
+      wait_vmcnt<IPT>();
+      asm volatile("s_barrier" ::: "memory");
+      // k-step 3: read the next tile's k-steps 0, 1
+      rd(SN{}, K0{});
+      rd(SN{}, K1{});
+      mm(K3{});
+      weave(std::integral_constant<int, 2 * NR>{}, K0{});
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    load_part(0, 0, 0, IPT);
+    load_part(1, min(1, KT - 1), 0, IPT);
+    wait_vmcnt<IPT>();
+    asm volatile("s_barrier" ::: "memory");
+    rd(I0{}, K0{});
+    rd(I0{}, K1{});
+    int kt = 0;
+    for (; kt + 1 < KT; kt += 2) {
+      tile2(I0{}, kt);
+      tile2(std::integral_constant<int, 1>{}, kt + 1);
+    }
+    if (kt < KT) tile2(I0{}, kt);
+    } else {
+    // One K tile in stage st: k-steps 0 .. KS-2 (each k-step's MFMAs alternate
+    // with the fragment reads of the next), then the barrier before the last
+    // k-step: after it this stage is free, and the first fragments of the next
+    // tile are read under the last k-step's MFMAs, so no wave idles between
+    // tiles.  The loads of tile kt + 2 into this stage are spread over LSPLIT
+    // k-steps -- the last one of this tile and the first LSPLIT - 1 of the
+    // next -- instead of leaving in one burst.  Loads past the last K tile
+    // fetch it again into a buffer nobody reads any more (no branches,
+    // constant wait counts).  The barrier is a bare s_barrier: a
+    // __syncthreads() fence would also drain the loads still in flight.
+    constexpr int LSPLIT = IPT % kLoadSplitK == 0 ? kLoadSplitK : 1;
+    static_assert(LSPLIT >= 1 && LSPLIT <= KS && IPT % LSPLIT == 0, "load split");
+    constexpr int QC = IPT / LSPLIT;  // load instructions per chunk
+    auto tile = [&](auto stc, int kt) __attribute__((always_inline)) {
+      constexpr int st = decltype(stc)::value;
       static_for<KS - 1>([&](auto kk) {
         constexpr int ks = decltype(kk)::value;
-        fload(st, ks + 1, (ks + 1) & 1);
+        read_frags(stc, std::integral_constant<int, ks + 1>{}, std::integral_constant<int, (ks + 1) & 1>{});
+        constexpr bool ld = ks + 1 < LSPLIT;
+        if constexpr (ld) load_part(st ^ 1, min(kt + 1, KT - 1), (ks + 1) * QC, (ks + 2) * QC);
         mfma_step(std::integral_constant<int, ks & 1>{});
+        constexpr int VP = ld ? (QC / NP > 0 ? QC / NP : 1) : 0;
         static_for<NP>([&](auto) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+          if constexpr (VP > 0) __builtin_amdgcn_sched_group_barrier(0x020, VP, 0);  // VMEM
           __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
         });
         if constexpr (NM > NP) __builtin_amdgcn_sched_group_barrier(0x008, NM - NP, 0);
         if constexpr (NR > NP) __builtin_amdgcn_sched_group_barrier(0x100, NR - NP, 0);
       });
-    };
-    // Every buffer is refilled right after the barrier that precedes its
-    // tile's last k-step, and the first fragments of the next tile are read
-    // under that k-step's MFMAs, so no wave idles between tiles.  Loads past
-    // the last K tile fetch the last tile again into a buffer nobody reads
-    // any more: the loop has no branches and constant wait counts.  The
-    // barrier is a bare s_barrier: a __syncthreads() fence would also drain
-    // the loads still in flight for later tiles.
-#pragma unroll
-    for (int t = 0; t < STAGES; ++t) dtl_load(min(t, KT - 1), t);
-    wait_vmcnt<(STAGES - 1) * IPT>();
-    asm volatile("s_barrier" ::: "memory");
-    fload(0, 0, 0);
-    for (int kt = 0; kt < KT - 1; ++kt) {
-      const int st = kt % STAGES;
-      inner_steps(st);
-      // own loads of tile kt + 1 done (later tiles stay in flight) and the
-      // last fragments of tile kt read; after the barrier tile kt + 1 is in
-      // LDS and nobody reads buffer st any more
-      wait_vmcnt<(STAGES - 2) * IPT>();
+      // own loads of tile kt + 1 done and the last fragments of tile kt read;
+      // after the barrier tile kt + 1 is in LDS and nobody reads stage st
+      wait_vmcnt<0>();
       __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
       asm volatile("s_barrier" ::: "memory");
-      dtl_load(min(kt + STAGES, KT - 1), st);
-      fload((kt + 1) % STAGES, 0, 0);
+      load_part(st, min(kt + 2, KT - 1), 0, QC);
+      read_frags(std::integral_constant<int, st ^ 1>{}, I0{}, I0{});
       mfma_step(std::integral_constant<int, (KS - 1) & 1>{});
-      constexpr int VP = IPT / NP > 0 ? IPT / NP : 1;
+      constexpr int VP = QC / NP > 0 ? QC / NP : 1;
       static_for<NP>([&](auto) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
         __builtin_amdgcn_sched_group_barrier(0x020, VP, 0);  // VMEM (buffer -> LDS)
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
       });
+    };
+    static_assert(STAGES == 2, "the unrolled loop alternates two stages");
+    using I1 = std::integral_constant<int, 1>;
+    load_part(0, 0, 0, IPT);
+    load_part(1, min(1, KT - 1), 0, QC);
+    wait_vmcnt<QC>();
+    asm volatile("s_barrier" ::: "memory");
+    read_frags(I0{}, I0{}, I0{});
+    int kt = 0;
+    for (; kt + 1 < KT; kt += 2) {
+      tile(I0{}, kt);
+      tile(I1{}, kt + 1);
     }
-    inner_steps((KT - 1) % STAGES);
-    mfma_step(std::integral_constant<int, (KS - 1) & 1>{});
+    if (kt < KT) tile(I0{}, kt);
+    }
+    // the refetches of the last tile must land before the epilogue reuses LDS
+    wait_vmcnt<0>();
     __syncthreads();
   } else {
     // ---- register path with zero-filled K tail (two LDS buffers).
@@ -386,26 +549,43 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
   });
 }
 
-template <int BM, int BN, int NWM, int NWN, int BK, int STAGES>
-hipError_t launch_cfg(const GemmProblem& p, hipStream_t s) {
-  const int tiles_n = (p.N + BN - 1) / BN;
-  long tiles = (long)((p.g[0].M + BM - 1) / BM) * tiles_n;
-  if (p.n_groups > 1) tiles += (long)((p.g[1].M + BM - 1) / BM) * tiles_n;
-  if (tiles == 0) return hipSuccess;
-  // direct-to-LDS path: whole K tiles, 16-byte aligned rows, and operands
-  // small enough for the 32-bit offsets of buffer loads
-  GemmProblem q = p;
-  q.dtl = 1;
+// direct-to-LDS path: whole K tiles, 16-byte aligned rows, and operands
+// small enough for the 32-bit offsets of buffer loads
+template <int BM, int BN, int BK>
+bool dtl_ok(const GemmProblem& p) {
   for (int g = 0; g < p.n_groups; ++g) {
     const GemmGroup& G = p.g[g];
     const bool ok = G.K % BK == 0 && G.lda % 8 == 0 && G.ldw % 8 == 0 && (long)(G.M + BM) * G.lda * 2 < (1L << 31) &&
                     (long)(p.N + BN) * G.ldw * 2 < (1L << 31);
-    if (!ok) q.dtl = 0;
+    if (!ok) return false;
   }
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, NWM, NWN, BK, STAGES>), dim3((unsigned)tiles), dim3(NWM * NWN * 64), 0,
-                     s, q);
+  return true;
+}
+
+template <int BM, int BN>
+long tile_count(const GemmProblem& p) {
+  const int tiles_n = (p.N + BN - 1) / BN;
+  long tiles = (long)((p.g[0].M + BM - 1) / BM) * tiles_n;
+  if (p.n_groups > 1) tiles += (long)((p.g[1].M + BM - 1) / BM) * tiles_n;
+  return tiles;
+}
+
+template <int BM, int BN, int NWM, int NWN, int BK, int STAGES, bool DTL>
+hipError_t launch_kernel(const GemmProblem& p, hipStream_t s) {
+  const long tiles = tile_count<BM, BN>(p);
+  if (tiles == 0) return hipSuccess;
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, NWM, NWN, BK, STAGES, DTL>), dim3((unsigned)tiles),
+                     dim3(NWM * NWN * 64), 0, s, p);
   return hipGetLastError();
 }
+
+template <int BM, int BN, int NWM, int NWN, int BK, int STAGES>
+hipError_t launch_cfg(const GemmProblem& p, hipStream_t s) {
+  if (dtl_ok<BM, BN, BK>(p)) return launch_kernel<BM, BN, NWM, NWN, BK, STAGES, true>(p, s);
+  return launch_kernel<BM, BN, NWM, NWN, BK, STAGES, false>(p, s);
+}
+
+constexpr bool kWaves4 = false;
 
 enum GemmCfg { CFG_128x64 = 0, CFG_256x256 = 1, CFG_128x128 = 2 };
 GemmCfg pick(const GemmProblem& p) {
@@ -428,7 +608,10 @@ hipError_t launch_gemm_bf16(const GemmProblem& p, hipStream_t s) {
     case CFG_128x64:
       return launch_cfg<128, 64, 4, 1, 64, 2>(p, s);
     case CFG_256x256:
-      return launch_cfg<256, 256, 4, 2, 64, 2>(p, s);
+      if (dtl_ok<256, 256, 64>(p))
+        return kWaves4 ? launch_kernel<256, 256, 2, 2, 64, 2, true>(p, s)
+                       : launch_kernel<256, 256, 4, 2, 64, 2, true>(p, s);
+      return launch_kernel<256, 256, 4, 2, 64, 2, false>(p, s);
     default:
       return launch_cfg<128, 128, 2, 2, 64, 2>(p, s);
   }
