@@ -26,6 +26,10 @@ namespace {
 constexpr int kLoadSplitK = 1;
 // main-loop schedule of the direct-to-LDS path (0: one barrier per K tile, 1: whole-tile register prefetch)
 constexpr int kSchedK = 1;
+// chunks in which the loads of one K tile leave (whole-tile prefetch schedule)
+constexpr int kLoadChunksK = 2;
+// 16x16x32 MFMAs in the whole-tile prefetch schedule (else 32x32x16)
+constexpr bool kMfma16K = true;
 
 struct TileCoord {
   int group, m0, n0;
@@ -108,6 +112,18 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
   const int wave = tid >> 6;
   const int wm = wave / NWN, wn = wave % NWN;
 
+  // 16x16x32 MFMAs (the whole-tile-prefetch direct-to-LDS path only): the
+  // 32x32 fragment (i, j) is the 2 x 2 block of 16x16 accumulators 2i.., 2j..
+  constexpr bool M16 = kMfma16K && DTL && kSchedK == 1;
+  f32x4_t acc16[M16 ? 2 * FM : 1][M16 ? 2 * FN : 1];
+  if constexpr (M16) {
+#pragma unroll
+    for (int i = 0; i < 2 * FM; ++i)
+#pragma unroll
+      for (int j = 0; j < 2 * FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc16[i][j][r] = 0.f;
+  }
   f32x16_t acc[FM][FN];
 #pragma unroll
   for (int i = 0; i < FM; ++i)
@@ -264,7 +280,90 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
     };
     constexpr int NR = FM + FN, NM = FM * FN, NP = NR < NM ? NR : NM;
     using I0 = std::integral_constant<int, 0>;
-    if constexpr (kSchedK == 1) {
+    if constexpr (M16) {
+    // ---- as below, with v_mfma_f32_16x16x32_bf16: two 32-wide k-steps per
+    // K tile, each split into two phases by fragment row; fragments of tile X
+    // are read in X-1's last phase (k-step 0) and X's first phase (k-step 1).
+    static_assert(BK == 64 && STAGES == 2, "schedule for 64-wide K tiles");
+    constexpr int FM2 = 2 * FM, FN2 = 2 * FN, NR2 = FM2 + FN2, NMP = FM * FN2;  // MFMAs per phase
+    static_assert((STAGES - 1) * A_STAGE + (FM2 - 1) * 16 * ROWB < 65536 &&
+                  (STAGES - 1) * B_STAGE + (FN2 - 1) * 16 * ROWB < 65536, "ds_read immediate offsets");
+    int fa16[2], fb16[2];
+    {
+      const int ra = wm * WTM + (lane & 15), rb = wn * WTN + (lane & 15);
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        fa16[ks] = lds_slot<CPR>(ra, 4 * ks + (lane >> 4)) * 16;
+        fb16[ks] = B_REGION + lds_slot<CPR>(rb, 4 * ks + (lane >> 4)) * 16;
+      }
+    }
+    bf16x8_t ha[2][FM2], hb[2][FN2];
+    auto rd16 = [&](auto stc, auto ksc) __attribute__((always_inline)) {
+      constexpr int st = decltype(stc)::value, ks = decltype(ksc)::value;
+#pragma unroll
+      for (int i = 0; i < FM2; ++i)
+        ha[ks][i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(lbase + fa16[ks] + st * A_STAGE + i * 16 * ROWB));
+#pragma unroll
+      for (int j = 0; j < FN2; ++j)
+        hb[ks][j] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(lbase + fb16[ks] + st * B_STAGE + j * 16 * ROWB));
+    };
+    auto mm16 = [&](auto ksc, auto hc) __attribute__((always_inline)) {
+      constexpr int ks = decltype(ksc)::value, h = decltype(hc)::value;
+#pragma unroll
+      for (int i = h * FM; i < (h + 1) * FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN2; ++j)
+          acc16[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ha[ks][i], hb[ks][j], acc16[i][j], 0, 0, 0);
+    };
+    auto weave16 = [&](auto rc, auto vc) __attribute__((always_inline)) {
+      constexpr int R = decltype(rc)::value, V = decltype(vc)::value;
+      static_for<NMP>([&](auto mc) {
+        constexpr int m = decltype(mc)::value;
+        constexpr int r = (m + 1) * R / NMP - m * R / NMP, v = (m + 1) * V / NMP - m * V / NMP;
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);
+        if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x020, v, 0);
+      });
+    };
+    constexpr int QH = IPT / 2;
+    using J0 = std::integral_constant<int, 0>;
+    using J1 = std::integral_constant<int, 1>;
+    auto tile16 = [&](auto stc, int kt) __attribute__((always_inline)) {
+      constexpr int st = decltype(stc)::value;
+      using SN = std::integral_constant<int, st ^ 1>;
+      rd16(stc, J1{});
+      mm16(J0{}, J0{});
+      weave16(std::integral_constant<int, NR2>{}, J0{});
+      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+      asm volatile("s_barrier" ::: "memory");
+      load_part(st, min(kt + 2, KT - 1), 0, QH);
+      mm16(J0{}, J1{});
+      weave16(J0{}, std::integral_constant<int, QH>{});
+      __builtin_amdgcn_sched_barrier(0);
+      load_part(st, min(kt + 2, KT - 1), QH, IPT);
+      mm16(J1{}, J0{});
+      weave16(J0{}, std::integral_constant<int, IPT - QH>{});
+      __builtin_amdgcn_sched_barrier(0);
+      wait_vmcnt<IPT>();
+      asm volatile("s_barrier" ::: "memory");
+      rd16(SN{}, J0{});
+      mm16(J1{}, J1{});
+      weave16(std::integral_constant<int, NR2>{}, J0{});
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    load_part(0, 0, 0, IPT);
+    load_part(1, min(1, KT - 1), 0, IPT);
+    wait_vmcnt<IPT>();
+    asm volatile("s_barrier" ::: "memory");
+    rd16(I0{}, J0{});
+    int kt = 0;
+    for (; kt + 1 < KT; kt += 2) {
+      tile16(I0{}, kt);
+      tile16(std::integral_constant<int, 1>{}, kt + 1);
+    }
+    if (kt < KT) tile16(I0{}, kt);
+    } else if constexpr (kSchedK == 1) {
     // ---- whole-tile register prefetch, two barriers per K tile.
     // Fragment registers hold one whole K tile (one buffer per k-step).  The
     // fragments of tile X are read during the last k-step of tile X-1 (k-steps
@@ -304,44 +403,52 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
         if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x020, v, 0);
       });
     };
-    constexpr int HALF = IPT / 2;
+    // the loads of tile kt + 2 leave in NCH equal chunks: k-steps 1, 2 (and 3,
+    // and the next tile's k-step 0) of tile kt
+    constexpr int NCH = IPT % kLoadChunksK == 0 ? kLoadChunksK : 2;
+    static_assert(NCH >= 2 && NCH <= 4 && IPT % NCH == 0, "load chunks");
+    constexpr int QC = IPT / NCH;
     using K0 = std::integral_constant<int, 0>;
     using K1 = std::integral_constant<int, 1>;
     using K2 = std::integral_constant<int, 2>;
     using K3 = std::integral_constant<int, 3>;
+    using RR = std::integral_constant<int, 2 * NR>;   // fragment reads of two k-steps
+    using VQ = std::integral_constant<int, QC>;
     auto tile2 = [&](auto stc, int kt) __attribute__((always_inline)) {
       constexpr int st = decltype(stc)::value;
       using SN = std::integral_constant<int, st ^ 1>;
-      // k-step 0: read this tile's k-steps 2, 3
+      // k-step 0: read this tile's k-steps 2, 3 (and the last chunk of tile kt + 1)
       rd(stc, K2{});
       rd(stc, K3{});
+      if constexpr (NCH == 4) load_part(st ^ 1, min(kt + 1, KT - 1), 3 * QC, IPT);
       mm(K0{});
-      weave(std::integral_constant<int, 2 * NR>{}, K0{});
+      weave(RR{}, std::integral_constant<int, NCH == 4 ? QC : 0>{});
       __builtin_amdgcn_sched_barrier(0);
       __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): own reads of this stage done
       asm volatile("s_barrier" ::: "memory");
       // k-steps 1, 2: loads of tile kt + 2 into this stage
-      load_part(st, min(kt + 2, KT - 1), 0, HALF);
+      load_part(st, min(kt + 2, KT - 1), 0, QC);
       mm(K1{});
-      weave(K0{}, std::integral_constant<int, HALF>{});
+      weave(K0{}, VQ{});
       __builtin_amdgcn_sched_barrier(0);
-      load_part(st, min(kt + 2, KT - 1), HALF, IPT);
+      load_part(st, min(kt + 2, KT - 1), QC, 2 * QC);
       mm(K2{});
-      weave(K0{}, std::integral_constant<int, IPT - HALF>{});
+      weave(K0{}, VQ{});
       __builtin_amdgcn_sched_barrier(0);
-      // tile kt + 1 landed (only the loads of kt + 2 may still be in flight)
-      wait_vmcnt<IPT>();
+      // tile kt + 1 landed (the chunks of kt + 2 issued so far may still be in flight)
+      wait_vmcnt<2 * QC>();
       asm volatile("s_barrier" ::: "memory");
       // k-step 3: read the next tile's k-steps 0, 1
       rd(SN{}, K0{});
       rd(SN{}, K1{});
+      if constexpr (NCH >= 3) load_part(st, min(kt + 2, KT - 1), 2 * QC, 3 * QC);
       mm(K3{});
-      weave(std::integral_constant<int, 2 * NR>{}, K0{});
+      weave(RR{}, std::integral_constant<int, NCH >= 3 ? QC : 0>{});
       __builtin_amdgcn_sched_barrier(0);
     };
     load_part(0, 0, 0, IPT);
-    load_part(1, min(1, KT - 1), 0, IPT);
-    wait_vmcnt<IPT>();
+    load_part(1, min(1, KT - 1), 0, NCH == 4 ? 3 * QC : IPT);
+    wait_vmcnt<NCH == 4 ? 3 * QC : IPT>();
     asm volatile("s_barrier" ::: "memory");
     rd(I0{}, K0{});
     rd(I0{}, K1{});
@@ -493,10 +600,25 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
     const bool vcols = E.mode == EPI_QKV && nb >= 2 * E.hidden && nb < 3 * E.hidden;
     static_for<FM>([&](auto ii) {
       constexpr int i = decltype(ii)::value;
-      static_for<16>([&](auto rr) {
-        constexpr int r = decltype(rr)::value;
-        stg[((r / 4) * 8 + (lane >> 5) * 4 + (r % 4)) * SP + (lane & 31)] = acc[i][j][r] + bn;
-      });
+      if constexpr (M16) {
+        static_for<2>([&](auto bb) {
+          constexpr int b = decltype(bb)::value;
+          const int nl16 = nb + b * 16 + (lane & 15);
+          const float bn16 = (bias != nullptr && nl16 < N) ? bf2f(bias[nl16]) : 0.f;
+          static_for<2>([&](auto aa) {
+            constexpr int a = decltype(aa)::value;
+            static_for<4>([&](auto rr) {
+              constexpr int r = decltype(rr)::value;
+              stg[(a * 16 + 4 * (lane >> 4) + r) * SP + b * 16 + (lane & 15)] = acc16[2 * i + a][2 * j + b][r] + bn16;
+            });
+          });
+        });
+      } else {
+        static_for<16>([&](auto rr) {
+          constexpr int r = decltype(rr)::value;
+          stg[((r / 4) * 8 + (lane >> 5) * 4 + (r % 4)) * SP + (lane & 31)] = acc[i][j][r] + bn;
+        });
+      }
       if (vcols) {
         const int rh = lane >> 5, c = lane & 31;
         float v[16];
