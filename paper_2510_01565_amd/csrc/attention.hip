@@ -161,7 +161,37 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
     // keep four fragment reads ahead of the MFMAs that consume them
     sched_read_ahead<2 * D / 16, 4>();
   };
-  // online softmax of tile j's scores, then O += P V
+  // Probabilities of one tile against the running max m_i, rounded to bf16 in
+  // the order the P V operand wants them (key pairs packed by one convert);
+  // returns this lane's sum of the rounded values (two bf16 products per
+  // v_dot2 with (1, 1)), which is also what O accumulates.
+  auto exps_pack = [&](const f32x16_t* s, bf16x8_t* pf) __attribute__((always_inline)) {
+    float t0 = 0.f, t1 = 0.f;
+    const bf16x2_t one = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      uint32_t w[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int i = (x & 1) * 8 + 2 * e;
+        // v_exp_f32 directly: results below 2^-126 flush to zero, which the
+        // softmax sum and the bf16 probabilities cannot tell from their true value
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[x >> 1][i], sl2, -m_i));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[x >> 1][i + 1], sl2, -m_i));
+        const bf16x2_t pk = {(__bf16)p0, (__bf16)p1};
+        if (e & 1) t1 = __builtin_amdgcn_fdot2_f32_bf16(pk, one, t1, false);
+        else t0 = __builtin_amdgcn_fdot2_f32_bf16(pk, one, t0, false);
+        w[e] = __builtin_bit_cast(uint32_t, pk);
+      }
+      pf[x] = __builtin_bit_cast(bf16x8_t, make_uint4(w[0], w[1], w[2], w[3]));
+    }
+    return t0 + t1;
+  };
+  // Online softmax of tile j's scores, then O += P V.  The probabilities are
+  // first taken against the current running max; only if some lane's sum
+  // exceeds 2^RESCALE_SLACK (or overflows, as on the first tile) is the true
+  // row max formed, the max raised, O and l rescaled, and the tile redone.
+  // O and l always share the max they were computed with, so O / l is exact.
   auto softmax_pv = [&](int j, int st, f32x16_t* s) {
     const int kv0 = j * BKV;
     if (kv0 + BKV > L) {
@@ -173,13 +203,15 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
           if (key >= L) s[kb][i] = -INFINITY;
         }
     }
-    float mx = s[0][0];
+    bf16x8_t pf[4];
+    float t = exps_pack(s, pf);
+    if (__any(!(t <= (float)(1 << (int)RESCALE_SLACK)))) {
+      float mx = s[0][0];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kb][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * sl2;
-    if (__any(mx > m_i + RESCALE_SLACK)) {
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kb][i]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * sl2;
       const float m_new = fmaxf(m_i, mx);
       const float alpha = __builtin_amdgcn_exp2f(m_i - m_new);
       m_i = m_new;
@@ -188,20 +220,9 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
       for (int db = 0; db < D / 32; ++db)
 #pragma unroll
         for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
+      t = exps_pack(s, pf);
     }
-    float ls = 0.f;
-    bf16x8_t pf[4];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        // v_exp_f32 directly: results below 2^-126 flush to zero, which the
-        // softmax sum and the bf16 probabilities cannot tell from their true value
-        const float p = __builtin_amdgcn_exp2f(fmaf(s[kb][i], sl2, -m_i));
-        ls += p;
-        pf[kb * 2 + (i >> 3)][i & 7] = (__bf16)p;
-      }
-    l_i += ls;
+    l_i += t;
     const uint4* V = smem[st] + KT_U4;
 #pragma unroll
     for (int ks2 = 0; ks2 < 4; ++ks2) {
@@ -376,6 +397,12 @@ hipError_t launch_attn_cfg(const AttnArgs& a, hipStream_t s) {
 // the plain order at 2 waves per SIMD, so the plain order with 2 buffers is used.
 hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s) {
   if (a.head_dim != D) return hipErrorInvalidValue;
+  // Many blocks: 128 queries per block, two blocks per CU, so the two waves of
+  // a SIMD belong to different blocks and drift apart (one in its softmax
+  // while the other issues MFMAs); +10% at 16 896 tokens.  Fewer blocks: 256
+  // queries per block, so the last round of blocks is fuller.
+  const AttnSched sc4 = make_sched(a.meta, 4 * 32);
+  if ((long)sc4.tile_off[sc4.n] * a.heads >= 2048) return launch_attn_cfg<4, 2, 0>(a, s);
   return launch_attn_cfg<8, 2, 0>(a, s);
 }
 

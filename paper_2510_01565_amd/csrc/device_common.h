@@ -26,6 +26,7 @@ __device__ __forceinline__ void static_for(F&& f) {
 
 typedef uint16_t bf16_t;  // raw bfloat16 storage
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 

@@ -22,14 +22,6 @@ namespace dit {
 
 namespace {
 
-// k-steps over which the loads of one K tile are spread (direct-to-LDS path)
-constexpr int kLoadSplitK = 1;
-// main-loop schedule of the direct-to-LDS path (0: one barrier per K tile, 1: whole-tile register prefetch)
-constexpr int kSchedK = 1;
-// chunks in which the loads of one K tile leave (whole-tile prefetch schedule)
-constexpr int kLoadChunksK = 2;
-// 16x16x32 MFMAs in the whole-tile prefetch schedule (else 32x32x16)
-constexpr bool kMfma16K = true;
 
 struct TileCoord {
   int group, m0, n0;
@@ -112,29 +104,29 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
   const int wave = tid >> 6;
   const int wm = wave / NWN, wn = wave % NWN;
 
-  // 16x16x32 MFMAs (the whole-tile-prefetch direct-to-LDS path only): the
-  // 32x32 fragment (i, j) is the 2 x 2 block of 16x16 accumulators 2i.., 2j..
-  constexpr bool M16 = kMfma16K && DTL && kSchedK == 1;
-  f32x4_t acc16[M16 ? 2 * FM : 1][M16 ? 2 * FN : 1];
-  if constexpr (M16) {
+  // Accumulators.  Direct-to-LDS path: 16x16 blocks, the 32x32 fragment
+  // (i, j) being the 2 x 2 blocks 2i.., 2j..; register path: 32x32 blocks.
+  constexpr int AM = DTL ? 2 * FM : 1, AN = DTL ? 2 * FN : 1;
+  constexpr int CM = DTL ? 1 : FM, CN = DTL ? 1 : FN;
+  f32x4_t acc16[AM][AN];
+  f32x16_t acc[CM][CN];
 #pragma unroll
-    for (int i = 0; i < 2 * FM; ++i)
+  for (int i = 0; i < AM; ++i)
 #pragma unroll
-      for (int j = 0; j < 2 * FN; ++j)
+    for (int j = 0; j < AN; ++j)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc16[i][j][r] = 0.f;
-  }
-  f32x16_t acc[FM][FN];
+      for (int r = 0; r < 4; ++r) acc16[i][j][r] = 0.f;
 #pragma unroll
-  for (int i = 0; i < FM; ++i)
+  for (int i = 0; i < CM; ++i)
 #pragma unroll
-    for (int j = 0; j < FN; ++j)
+    for (int j = 0; j < CN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int KT = (K + BK - 1) / BK;
 
-  // fragments of k-step ks (16 wide) of stage st: lane row (lane & 31), chunk 2 ks + lane / 32
+  // register path: fragments of k-step ks (16 wide) of stage st: lane row
+  // (lane & 31), chunk 2 ks + lane / 32
   bf16x8_t fa[2][FM], fb[2][FN];
   auto fload = [&](int st, int ks, int buf) {
     const int ch = ks * 2 + (lane >> 5);
@@ -179,8 +171,8 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
   };
 
   if (DTL) {  // a compile-time constant: the other path is dropped
-    // ---- direct-to-LDS ring.  LDS holds [A stage 0 .. STAGES-1 | B stage 0 ..
-    // STAGES-1], rows of BK bf16 (CPR 16-byte chunks, XOR-swizzled).  Wave
+    // ---- direct-to-LDS ring.  LDS holds [A stage 0 | A stage 1 | B stage 0 |
+    // B stage 1], rows of BK bf16 (CPR 16-byte chunks, XOR-swizzled).  Wave
     // instruction q of a tile moves 64 lanes x 16 bytes = RPI tile rows; lane l
     // fills slot l % CPR of row l / CPR and so fetches the logical chunk that
     // the swizzle puts in that slot.  Loads are range-checked buffer loads
@@ -192,18 +184,31 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
     // the LDS destination of each instruction (scalar, wave-uniform) and the
     // lane's LDS fragment address for each k-step (the stage and fragment
     // index are immediate offsets), so the loop issues MFMAs, LDS reads and
-    // buffer loads and almost no vector ALU work.
+    // buffer loads and no vector ALU work.
+    //
+    // MFMAs are v_mfma_f32_16x16x32_bf16: a 64-wide K tile is two 32-wide
+    // k-steps, each split into two phases by fragment row, four phases of
+    // FM x 2FN MFMAs.  Fragment registers hold one whole K tile.  Tile X is
+    // read in the last phase of X-1 (k-step 0) and the first phase of X
+    // (k-step 1); a barrier after X's first phase frees X's stage and the
+    // loads of tile X+2 into it leave over phases 1 and 2 (one per two MFMAs,
+    // about what the texture path drains); a second barrier before the last
+    // phase makes tile X+1 visible.  A load thus has about one K tile between
+    // its issue and the barrier that needs it.
+    static_assert(BK == 64 && STAGES == 2, "schedule for 64-wide K tiles, two stages");
     constexpr int RPI = 64 / CPR;                       // tile rows per instruction
     constexpr int AI = BM / RPI / NWAVES, BI = BN / RPI / NWAVES;
     static_assert(AI * RPI * NWAVES == BM && BI * RPI * NWAVES == BN, "tile config");
     constexpr int IPT = AI + BI;                        // load instructions per tile per wave
-    constexpr int KS = BK / 16;                         // k-steps per tile
     constexpr int ROWB = CPR * 16;                      // bytes per LDS row
     constexpr int A_STAGE = BM * ROWB, B_STAGE = BN * ROWB;
     constexpr int B_REGION = STAGES * A_STAGE;
+    constexpr int FM2 = 2 * FM, FN2 = 2 * FN;           // 16-row fragments per wave tile
+    constexpr int NR2 = FM2 + FN2;                      // fragment reads per k-step
+    constexpr int NMP = FM * FN2;                       // MFMAs per phase
     static_assert(B_REGION + STAGES * B_STAGE <= (int)sizeof(lds), "LDS");
-    static_assert((STAGES - 1) * A_STAGE + (FM - 1) * 32 * ROWB < 65536 &&
-                  (STAGES - 1) * B_STAGE + (FN - 1) * 32 * ROWB < 65536, "ds_read immediate offsets");
+    static_assert((STAGES - 1) * A_STAGE + (FM2 - 1) * 16 * ROWB < 65536 &&
+                  (STAGES - 1) * B_STAGE + (FN2 - 1) * 16 * ROWB < 65536, "ds_read immediate offsets");
     const int wv = __builtin_amdgcn_readfirstlane(wave);  // wave index in a scalar register
     const __amdgpu_buffer_rsrc_t rsa = __builtin_amdgcn_make_buffer_rsrc((void*)A, (short)0, (int)((long)M * lda * 2),
                                                                          kBufferWord3);
@@ -226,15 +231,16 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
         gob[q] = ((n0 + row) * (int)ldw + kc * 8) * 2;
       }
     }
-    // per-lane LDS byte address of fragment 0 at k-step ks, stage 0.  Rows of
-    // fragment i differ by 32 i, which leaves the swizzle term unchanged.
-    int fra[KS], frb[KS];
+    // per-lane LDS byte address of fragment 0 at k-step ks, stage 0: row
+    // lane % 16, chunk 4 ks + lane / 16.  Rows of fragment i differ by 16 i,
+    // which leaves the swizzle term unchanged.
+    int fra[2], frb[2];
     {
-      const int ra = wm * WTM + (lane & 31), rb = wn * WTN + (lane & 31);
+      const int ra = wm * WTM + (lane & 15), rb = wn * WTN + (lane & 15);
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        fra[ks] = lds_slot<CPR>(ra, 2 * ks + (lane >> 5)) * 16;
-        frb[ks] = B_REGION + lds_slot<CPR>(rb, 2 * ks + (lane >> 5)) * 16;
+      for (int ks = 0; ks < 2; ++ks) {
+        fra[ks] = lds_slot<CPR>(ra, 4 * ks + (lane >> 4)) * 16;
+        frb[ks] = B_REGION + lds_slot<CPR>(rb, 4 * ks + (lane >> 4)) * 16;
       }
     }
     char* const lbase = (char*)lds;
@@ -261,53 +267,18 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
             16, vo, koff, 0, 0);
       }
     };
-    auto read_frags = [&](auto stc, auto ksc, auto bufc) __attribute__((always_inline)) {
-      constexpr int st = decltype(stc)::value, ks = decltype(ksc)::value, buf = decltype(bufc)::value;
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-        fa[buf][i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(lbase + fra[ks] + st * A_STAGE + i * 32 * ROWB));
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-        fb[buf][j] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(lbase + frb[ks] + st * B_STAGE + j * 32 * ROWB));
-    };
-    auto mfma_step = [&](auto bufc) __attribute__((always_inline)) {
-      constexpr int buf = decltype(bufc)::value;
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][i], fb[buf][j], acc[i][j], 0, 0, 0);
-    };
-    constexpr int NR = FM + FN, NM = FM * FN, NP = NR < NM ? NR : NM;
-    using I0 = std::integral_constant<int, 0>;
-    if constexpr (M16) {
-    // ---- as below, with v_mfma_f32_16x16x32_bf16: two 32-wide k-steps per
-    // K tile, each split into two phases by fragment row; fragments of tile X
-    // are read in X-1's last phase (k-step 0) and X's first phase (k-step 1).
-    static_assert(BK == 64 && STAGES == 2, "schedule for 64-wide K tiles");
-    constexpr int FM2 = 2 * FM, FN2 = 2 * FN, NR2 = FM2 + FN2, NMP = FM * FN2;  // MFMAs per phase
-    static_assert((STAGES - 1) * A_STAGE + (FM2 - 1) * 16 * ROWB < 65536 &&
-                  (STAGES - 1) * B_STAGE + (FN2 - 1) * 16 * ROWB < 65536, "ds_read immediate offsets");
-    int fa16[2], fb16[2];
-    {
-      const int ra = wm * WTM + (lane & 15), rb = wn * WTN + (lane & 15);
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        fa16[ks] = lds_slot<CPR>(ra, 4 * ks + (lane >> 4)) * 16;
-        fb16[ks] = B_REGION + lds_slot<CPR>(rb, 4 * ks + (lane >> 4)) * 16;
-      }
-    }
     bf16x8_t ha[2][FM2], hb[2][FN2];
-    auto rd16 = [&](auto stc, auto ksc) __attribute__((always_inline)) {
+    auto rd = [&](auto stc, auto ksc) __attribute__((always_inline)) {
       constexpr int st = decltype(stc)::value, ks = decltype(ksc)::value;
 #pragma unroll
       for (int i = 0; i < FM2; ++i)
-        ha[ks][i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(lbase + fa16[ks] + st * A_STAGE + i * 16 * ROWB));
+        ha[ks][i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(lbase + fra[ks] + st * A_STAGE + i * 16 * ROWB));
 #pragma unroll
       for (int j = 0; j < FN2; ++j)
-        hb[ks][j] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(lbase + fb16[ks] + st * B_STAGE + j * 16 * ROWB));
+        hb[ks][j] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(lbase + frb[ks] + st * B_STAGE + j * 16 * ROWB));
     };
-    auto mm16 = [&](auto ksc, auto hc) __attribute__((always_inline)) {
+    // phase h of k-step ks: fragment rows h FM .. (h + 1) FM - 1
+    auto mm = [&](auto ksc, auto hc) __attribute__((always_inline)) {
       constexpr int ks = decltype(ksc)::value, h = decltype(hc)::value;
 #pragma unroll
       for (int i = h * FM; i < (h + 1) * FM; ++i)
@@ -315,209 +286,64 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
         for (int j = 0; j < FN2; ++j)
           acc16[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ha[ks][i], hb[ks][j], acc16[i][j], 0, 0, 0);
     };
-    auto weave16 = [&](auto rc, auto vc) __attribute__((always_inline)) {
+    // instruction order of a phase: each MFMA followed by its share of R LDS
+    // reads and V buffer loads
+    auto weave = [&](auto rc, auto vc) __attribute__((always_inline)) {
       constexpr int R = decltype(rc)::value, V = decltype(vc)::value;
       static_for<NMP>([&](auto mc) {
         constexpr int m = decltype(mc)::value;
         constexpr int r = (m + 1) * R / NMP - m * R / NMP, v = (m + 1) * V / NMP - m * V / NMP;
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);
-        if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x020, v, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                           // MFMA
+        if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);      // DS read
+        if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x020, v, 0);      // VMEM read
       });
     };
     constexpr int QH = IPT / 2;
     using J0 = std::integral_constant<int, 0>;
     using J1 = std::integral_constant<int, 1>;
-    auto tile16 = [&](auto stc, int kt) __attribute__((always_inline)) {
+    auto tile = [&](auto stc, int kt) __attribute__((always_inline)) {
       constexpr int st = decltype(stc)::value;
       using SN = std::integral_constant<int, st ^ 1>;
-      rd16(stc, J1{});
-      mm16(J0{}, J0{});
-      weave16(std::integral_constant<int, NR2>{}, J0{});
+      // phase 0: this tile's k-step 1 fragments
+      rd(stc, J1{});
+      mm(J0{}, J0{});
+      weave(std::integral_constant<int, NR2>{}, J0{});
       __builtin_amdgcn_sched_barrier(0);
-      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): own reads of this stage done
       asm volatile("s_barrier" ::: "memory");
+      // phases 1, 2: the loads of tile kt + 2 into this stage
       load_part(st, min(kt + 2, KT - 1), 0, QH);
-      mm16(J0{}, J1{});
-      weave16(J0{}, std::integral_constant<int, QH>{});
+      mm(J0{}, J1{});
+      weave(J0{}, std::integral_constant<int, QH>{});
       __builtin_amdgcn_sched_barrier(0);
       load_part(st, min(kt + 2, KT - 1), QH, IPT);
-      mm16(J1{}, J0{});
-      weave16(J0{}, std::integral_constant<int, IPT - QH>{});
+      mm(J1{}, J0{});
+      weave(J0{}, std::integral_constant<int, IPT - QH>{});
       __builtin_amdgcn_sched_barrier(0);
+      // tile kt + 1 landed (only the loads of kt + 2 may still be in flight)
       wait_vmcnt<IPT>();
       asm volatile("s_barrier" ::: "memory");
-      rd16(SN{}, J0{});
-      mm16(J1{}, J1{});
-      weave16(std::integral_constant<int, NR2>{}, J0{});
+      // phase 3: the next tile's k-step 0 fragments
+      rd(SN{}, J0{});
+      mm(J1{}, J1{});
+      weave(std::integral_constant<int, NR2>{}, J0{});
       __builtin_amdgcn_sched_barrier(0);
     };
+    // Loads past the last K tile fetch it again into a stage nobody reads any
+    // more (no branches, constant wait counts).  The barriers are bare
+    // s_barriers: a __syncthreads() fence would also drain the loads still in
+    // flight for later tiles.
     load_part(0, 0, 0, IPT);
     load_part(1, min(1, KT - 1), 0, IPT);
     wait_vmcnt<IPT>();
     asm volatile("s_barrier" ::: "memory");
-    rd16(I0{}, J0{});
+    rd(J0{}, J0{});
     int kt = 0;
     for (; kt + 1 < KT; kt += 2) {
-      tile16(I0{}, kt);
-      tile16(std::integral_constant<int, 1>{}, kt + 1);
+      tile(J0{}, kt);
+      tile(J1{}, kt + 1);
     }
-    if (kt < KT) tile16(I0{}, kt);
-    } else if constexpr (kSchedK == 1) {
-    // ---- whole-tile register prefetch, two barriers per K tile.
-    // Fragment registers hold one whole K tile (one buffer per k-step).  The
-    // fragments of tile X are read during the last k-step of tile X-1 (k-steps
-    // 0, 1) and the first k-step of X (k-steps 2, 3); after a barrier at the
-    // start of X's second k-step nobody reads X's stage any more and the loads
-    // of tile X+2 into it are issued over X's k-steps 1 and 2 (about the rate
-    // the texture path drains them); a second barrier before X's last k-step
-    // makes tile X+1 visible.  A load thus has about one K tile between its
-    // issue and the barrier that needs it.
-    static_assert(KS == 4 && STAGES == 2, "schedule for 64-wide K tiles");
-    bf16x8_t ga[KS][FM], gb[KS][FN];
-    auto rd = [&](auto stc, auto ksc) __attribute__((always_inline)) {
-      constexpr int st = decltype(stc)::value, ks = decltype(ksc)::value;
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-        ga[ks][i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(lbase + fra[ks] + st * A_STAGE + i * 32 * ROWB));
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-        gb[ks][j] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(lbase + frb[ks] + st * B_STAGE + j * 32 * ROWB));
-    };
-    auto mm = [&](auto ksc) __attribute__((always_inline)) {
-      constexpr int ks = decltype(ksc)::value;
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga[ks][i], gb[ks][j], acc[i][j], 0, 0, 0);
-    };
-    // interleave: NM MFMAs with R DS reads and V VMEM loads spread evenly
-    auto weave = [&](auto rc, auto vc) __attribute__((always_inline)) {
-      constexpr int R = decltype(rc)::value, V = decltype(vc)::value;
-      static_for<NM>([&](auto mc) {
-        constexpr int m = decltype(mc)::value;
-        constexpr int r = (m + 1) * R / NM - m * R / NM, v = (m + 1) * V / NM - m * V / NM;
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);
-        if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x020, v, 0);
-      });
-    };
-    // the loads of tile kt + 2 leave in NCH equal chunks: k-steps 1, 2 (and 3,
-    // and the next tile's k-step 0) of tile kt
-    constexpr int NCH = IPT % kLoadChunksK == 0 ? kLoadChunksK : 2;
-    static_assert(NCH >= 2 && NCH <= 4 && IPT % NCH == 0, "load chunks");
-    constexpr int QC = IPT / NCH;
-    using K0 = std::integral_constant<int, 0>;
-    using K1 = std::integral_constant<int, 1>;
-    using K2 = std::integral_constant<int, 2>;
-    using K3 = std::integral_constant<int, 3>;
-    using RR = std::integral_constant<int, 2 * NR>;   // fragment reads of two k-steps
-    using VQ = std::integral_constant<int, QC>;
-    auto tile2 = [&](auto stc, int kt) __attribute__((always_inline)) {
-      constexpr int st = decltype(stc)::value;
-      using SN = std::integral_constant<int, st ^ 1>;
-      // k-step 0: read this tile's k-steps 2, 3 (and the last chunk of tile kt + 1)
-      rd(stc, K2{});
-      rd(stc, K3{});
-      if constexpr (NCH == 4) load_part(st ^ 1, min(kt + 1, KT - 1), 3 * QC, IPT);
-      mm(K0{});
-      weave(RR{}, std::integral_constant<int, NCH == 4 ? QC : 0>{});
-      __builtin_amdgcn_sched_barrier(0);
-      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): own reads of this stage done
-      asm volatile("s_barrier" ::: "memory");
-      // k-steps 1, 2: loads of tile kt + 2 into this stage
-      load_part(st, min(kt + 2, KT - 1), 0, QC);
-      mm(K1{});
-      weave(K0{}, VQ{});
-      __builtin_amdgcn_sched_barrier(0);
-      load_part(st, min(kt + 2, KT - 1), QC, 2 * QC);
-      mm(K2{});
-      weave(K0{}, VQ{});
-      __builtin_amdgcn_sched_barrier(0);
-      // tile kt + 1 landed (the chunks of kt + 2 issued so far may still be in flight)
-      wait_vmcnt<2 * QC>();
-      asm volatile("s_barrier" ::: "memory");
-      // k-step 3: read the next tile's k-steps 0, 1
-      rd(SN{}, K0{});
-      rd(SN{}, K1{});
-      if constexpr (NCH >= 3) load_part(st, min(kt + 2, KT - 1), 2 * QC, 3 * QC);
-      mm(K3{});
-      weave(RR{}, std::integral_constant<int, NCH >= 3 ? QC : 0>{});
-      __builtin_amdgcn_sched_barrier(0);
-    };
-    load_part(0, 0, 0, IPT);
-    load_part(1, min(1, KT - 1), 0, NCH == 4 ? 3 * QC : IPT);
-    wait_vmcnt<NCH == 4 ? 3 * QC : IPT>();
-    asm volatile("s_barrier" ::: "memory");
-    rd(I0{}, K0{});
-    rd(I0{}, K1{});
-    int kt = 0;
-    for (; kt + 1 < KT; kt += 2) {
-      tile2(I0{}, kt);
-      tile2(std::integral_constant<int, 1>{}, kt + 1);
-    }
-    if (kt < KT) tile2(I0{}, kt);
-    } else {
-    // One K tile in stage st: k-steps 0 .. KS-2 (each k-step's MFMAs alternate
-    // with the fragment reads of the next), then the barrier before the last
-    // k-step: after it this stage is free, and the first fragments of the next
-    // tile are read under the last k-step's MFMAs, so no wave idles between
-    // tiles.  The loads of tile kt + 2 into this stage are spread over LSPLIT
-    // k-steps -- the last one of this tile and the first LSPLIT - 1 of the
-    // next -- instead of leaving in one burst.  Loads past the last K tile
-    // fetch it again into a buffer nobody reads any more (no branches,
-    // constant wait counts).  The barrier is a bare s_barrier: a
-    // __syncthreads() fence would also drain the loads still in flight.
-    constexpr int LSPLIT = IPT % kLoadSplitK == 0 ? kLoadSplitK : 1;
-    static_assert(LSPLIT >= 1 && LSPLIT <= KS && IPT % LSPLIT == 0, "load split");
-    constexpr int QC = IPT / LSPLIT;  // load instructions per chunk
-    auto tile = [&](auto stc, int kt) __attribute__((always_inline)) {
-      constexpr int st = decltype(stc)::value;
-      static_for<KS - 1>([&](auto kk) {
-        constexpr int ks = decltype(kk)::value;
-        read_frags(stc, std::integral_constant<int, ks + 1>{}, std::integral_constant<int, (ks + 1) & 1>{});
-        constexpr bool ld = ks + 1 < LSPLIT;
-        if constexpr (ld) load_part(st ^ 1, min(kt + 1, KT - 1), (ks + 1) * QC, (ks + 2) * QC);
-        mfma_step(std::integral_constant<int, ks & 1>{});
-        constexpr int VP = ld ? (QC / NP > 0 ? QC / NP : 1) : 0;
-        static_for<NP>([&](auto) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-          if constexpr (VP > 0) __builtin_amdgcn_sched_group_barrier(0x020, VP, 0);  // VMEM
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
-        });
-        if constexpr (NM > NP) __builtin_amdgcn_sched_group_barrier(0x008, NM - NP, 0);
-        if constexpr (NR > NP) __builtin_amdgcn_sched_group_barrier(0x100, NR - NP, 0);
-      });
-      // own loads of tile kt + 1 done and the last fragments of tile kt read;
-      // after the barrier tile kt + 1 is in LDS and nobody reads stage st
-      wait_vmcnt<0>();
-      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
-      asm volatile("s_barrier" ::: "memory");
-      load_part(st, min(kt + 2, KT - 1), 0, QC);
-      read_frags(std::integral_constant<int, st ^ 1>{}, I0{}, I0{});
-      mfma_step(std::integral_constant<int, (KS - 1) & 1>{});
-      constexpr int VP = QC / NP > 0 ? QC / NP : 1;
-      static_for<NP>([&](auto) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x020, VP, 0);  // VMEM (buffer -> LDS)
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
-      });
-    };
-    static_assert(STAGES == 2, "the unrolled loop alternates two stages");
-    using I1 = std::integral_constant<int, 1>;
-    load_part(0, 0, 0, IPT);
-    load_part(1, min(1, KT - 1), 0, QC);
-    wait_vmcnt<QC>();
-    asm volatile("s_barrier" ::: "memory");
-    read_frags(I0{}, I0{}, I0{});
-    int kt = 0;
-    for (; kt + 1 < KT; kt += 2) {
-      tile(I0{}, kt);
-      tile(I1{}, kt + 1);
-    }
-    if (kt < KT) tile(I0{}, kt);
-    }
+    if (kt < KT) tile(J0{}, kt);
     // the refetches of the last tile must land before the epilogue reuses LDS
     wait_vmcnt<0>();
     __syncthreads();
@@ -600,7 +426,7 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
     const bool vcols = E.mode == EPI_QKV && nb >= 2 * E.hidden && nb < 3 * E.hidden;
     static_for<FM>([&](auto ii) {
       constexpr int i = decltype(ii)::value;
-      if constexpr (M16) {
+      if constexpr (DTL) {
         static_for<2>([&](auto bb) {
           constexpr int b = decltype(bb)::value;
           const int nl16 = nb + b * 16 + (lane & 15);
@@ -707,8 +533,6 @@ hipError_t launch_cfg(const GemmProblem& p, hipStream_t s) {
   return launch_kernel<BM, BN, NWM, NWN, BK, STAGES, false>(p, s);
 }
 
-constexpr bool kWaves4 = false;
-
 enum GemmCfg { CFG_128x64 = 0, CFG_256x256 = 1, CFG_128x128 = 2 };
 GemmCfg pick(const GemmProblem& p) {
   int maxM = p.g[0].M;
@@ -730,10 +554,7 @@ hipError_t launch_gemm_bf16(const GemmProblem& p, hipStream_t s) {
     case CFG_128x64:
       return launch_cfg<128, 64, 4, 1, 64, 2>(p, s);
     case CFG_256x256:
-      if (dtl_ok<256, 256, 64>(p))
-        return kWaves4 ? launch_kernel<256, 256, 2, 2, 64, 2, true>(p, s)
-                       : launch_kernel<256, 256, 4, 2, 64, 2, true>(p, s);
-      return launch_kernel<256, 256, 4, 2, 64, 2, false>(p, s);
+      return launch_cfg<256, 256, 4, 2, 64, 2>(p, s);
     default:
       return launch_cfg<128, 128, 2, 2, 64, 2>(p, s);
   }
