@@ -345,10 +345,13 @@ def main() -> int:
     log(f"{wl.name}: {main_res['ms_per_step']:.2f} ms/step, {main_res['tflops']:.1f} TFLOP/s "
         f"({100 * main_res['frac_peak']:.1f}% of peak), CV {main_res['cv_pct']:.2f}%")
     per = {wl.name: {k: v for k, v in main_res.items() if k != "kernels"}}
+    models = {wl.model: (cfg, w)}
     for name in [x for x in args.extra.split(",") if x]:
         ow = workloads.WORKLOADS[name]
-        if ow.model != wl.model:
-            continue
+        if ow.model not in models:
+            # another model shape (e.g. the SD3-Medium one): its own seeded weights
+            models[ow.model] = make_model(torch, dit, synth, ow.model, args.seed, dev)
+        cfg, w = models[ow.model]
         if ow.kind == "attention_share":
             r = run_sp_share(torch, dit, synth, workloads, ow, cfg, w, args.extra_steps, args.seed, dev)
             log(f"{name}: {r['ms_per_step']:.2f} ms per share step, {r['tflops']:.1f} TFLOP/s ({r['note']})")

@@ -71,7 +71,7 @@ typedef enum { DIT_F32 = 0, DIT_BF16 = 1 } dit_dtype;
 typedef struct {
   int hidden;        /* H, a multiple of 64 */
   int heads;         /* heads * head_dim == hidden */
-  int head_dim;      /* 128 (bf16 or f32) or 64 (f32) */
+  int head_dim;      /* bf16: 128 or 64; f32: 64 */
   int mlp_ratio;     /* MLP width = mlp_ratio * hidden */
   int n_double;
   int n_single;

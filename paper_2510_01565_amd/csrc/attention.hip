@@ -2,7 +2,7 @@
 // request, never materialising the L x L score matrix (online softmax over
 // 64-key tiles).
 //
-// bf16 kernel (head_dim 128) on the gfx950 matrix cores.  Each wavefront owns
+// bf16 kernel (head_dim 128 or 64) on the gfx950 matrix cores.  Each wavefront owns
 // 32 queries.  It computes the transposed score tile S^T = K Q^T with
 // v_mfma_f32_32x32x16_bf16, so every lane holds the scores of ONE query
 // (column lane % 32) for half of the keys: the row max and row sum are
@@ -30,7 +30,6 @@ struct AttnSched {
 };
 
 constexpr int BKV = 64;  // keys per tile
-constexpr int D = 128;
 // Lazy rescaling: the running max used for exp2 is only raised when a new
 // score exceeds it by more than 2^RESCALE_SLACK; until then probabilities may
 // reach 2^8, which fp32 and bf16 hold exactly as well as any other value.
@@ -53,25 +52,26 @@ __device__ __forceinline__ void sched_read_ahead() {
 // s_waitcnt with vmcnt = 0 and the other counters left alone (gfx9 encoding).
 __device__ __forceinline__ void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); }
 
-// NW waves x 32 queries per block.
+// NW waves x 32 queries per block, head dimension HD (64 or 128).
 //
 // Pipeline over 64-key tiles j: K and V^T tiles arrive by direct-to-LDS loads
 // (global_load_lds_dwordx4) in a ring of STAGES buffers, issued STAGES - 1
-// tiles ahead.  With PIPE the score MFMAs of tile j + 1 are issued before the
-// softmax of tile j (matrix cores on S(j + 1) while the vector ALUs
-// exponentiate tile j); without it each tile runs scores, softmax, P V.
-// PIPE: issue the next tile's score MFMAs before this tile's softmax.
-// PRIO: raise the wave priority while it issues MFMAs.
-template <int NW, int STAGES = 3, int PIPE = 1, int PRIO = 0>
+// tiles ahead; each tile runs scores, softmax, P V in turn.
+template <int NW, int HD, int STAGES>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
   constexpr int BQ = NW * 32;
-  static_assert(STAGES >= 2 + PIPE, "the score pipeline reads tile j + 1 while tile j + 2 loads");
-  constexpr int KT_U4 = BKV * 16;  // K tile: [64 keys][16 chunks of 8 d], chunk slot ^= key & 15
-  constexpr int VT_U4 = D * 8;     // V^T tile: [128 d][8 chunks of 8 key slots], chunk slot ^= (d >> 1) & 7
-  constexpr int KI = BKV / 4 / NW; // K-tile load instructions per wave (4 keys each)
-  constexpr int VI = D / 8 / NW;   // V^T-tile load instructions per wave (8 rows each)
-  static_assert(KI * 4 * NW == BKV && VI * 8 * NW == D, "tile config");
+  static_assert(HD == 64 || HD == 128, "head dim");
+  constexpr int CH = HD / 8;       // 16-byte chunks per key row of the K tile
+  constexpr int KPI = 64 / CH;     // keys per load instruction (64 lanes x 16 bytes)
+  constexpr int KT_U4 = BKV * CH;  // K tile: [64 keys][CH chunks of 8 d], chunk slot swizzled by kswz
+  constexpr int VT_U4 = HD * 8;    // V^T tile: [HD d][8 chunks of 8 key slots], chunk slot ^= (d >> 1) & 7
+  constexpr int KI = BKV / KPI / NW;  // K-tile load instructions per wave
+  constexpr int VI = HD / 8 / NW;     // V^T-tile load instructions per wave (8 rows each)
+  static_assert(KI * KPI * NW == BKV && VI * 8 * NW == HD, "tile config");
+  // slot of chunk c in key row `key`: the 16 keys one ds_read_b128 serves per
+  // cycle land on 16 different 16-byte bank groups (an involution in c)
+  auto kswz = [](int key, int c) { return HD == 128 ? c ^ (key & 15) : c ^ ((key >> 1) & 7); };
   __shared__ uint4 smem[STAGES][KT_U4 + VT_U4];
 
   const int per_head = sc.tile_off[sc.n];
@@ -98,10 +98,10 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
     uint4* S = smem[st];
 #pragma unroll
     for (int q = 0; q < KI; ++q) {
-      const int k0 = (wave * KI + q) * 4;
-      const int key = k0 + (lane >> 4), sl = lane & 15;
-      const bf16_t* g = Kg + (long)min(kv0 + key, L - 1) * a.k_tok + (sl ^ (key & 15)) * 8;
-      __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)(S + k0 * 16), 16, 0,
+      const int k0 = (wave * KI + q) * KPI;
+      const int key = k0 + lane / CH, sl = lane % CH;
+      const bf16_t* g = Kg + (long)min(kv0 + key, L - 1) * a.k_tok + kswz(key, sl) * 8;
+      __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)(S + k0 * CH), 16, 0,
                                        0);
     }
 #pragma unroll
@@ -115,25 +115,24 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
   };
 
   const int ntiles = (L + BKV - 1) / BKV;
-  // prologue: the first STAGES - 1 tiles in flight (the pipelined form also needs
-  // tile j + 1 resident at step j, hence one buffer more than it has in flight)
+  // prologue: the first STAGES - 1 tiles in flight
 #pragma unroll
   for (int t = 0; t < STAGES - 1; ++t)
     if (t < ntiles) tile_load(t, t);
 
   // Q fragments (B operand of S^T = K Q^T): query q0 + wave*32 + lane%32, d chunk 2*ks + lane/32
   const int qrow = q0 + wave * 32 + (lane & 31);
-  bf16x8_t qf[D / 16];
+  bf16x8_t qf[HD / 16];
 #pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) {
+  for (int ks = 0; ks < HD / 16; ++ks) {
     uint4 u = make_uint4(0, 0, 0, 0);
     if (qrow < L) u = *(const uint4*)(Qg + (long)qrow * a.q_tok + (ks * 2 + hl) * 8);
     qf[ks] = __builtin_bit_cast(bf16x8_t, u);
   }
 
-  f32x16_t o[D / 32];
+  f32x16_t o[HD / 32];
 #pragma unroll
-  for (int db = 0; db < D / 32; ++db)
+  for (int db = 0; db < HD / 32; ++db)
 #pragma unroll
     for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
   float m_i = -INFINITY, l_i = 0.f;
@@ -143,23 +142,21 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
   // register i, query lane % 32)
   auto scores = [&](int st, f32x16_t* s) {
     const uint4* S = smem[st];
-    if constexpr (PRIO) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int i = 0; i < 16; ++i) s[kb][i] = 0.f;
 #pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) {
+    for (int ks = 0; ks < HD / 16; ++ks) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
         const int key = kb * 32 + (lane & 31);
-        const uint4 u = S[key * 16 + ((ks * 2 + hl) ^ (key & 15))];
+        const uint4 u = S[key * CH + kswz(key, ks * 2 + hl)];
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, u), qf[ks], s[kb], 0, 0, 0);
       }
     }
-    if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
     // keep four fragment reads ahead of the MFMAs that consume them
-    sched_read_ahead<2 * D / 16, 4>();
+    sched_read_ahead<2 * HD / 16, 4>();
   };
   // Probabilities of one tile against the running max m_i, rounded to bf16 in
   // the order the P V operand wants them (key pairs packed by one convert);
@@ -217,7 +214,7 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
       m_i = m_new;
       l_i *= alpha;
 #pragma unroll
-      for (int db = 0; db < D / 32; ++db)
+      for (int db = 0; db < HD / 32; ++db)
 #pragma unroll
         for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
       t = exps_pack(s, pf);
@@ -227,45 +224,22 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
 #pragma unroll
     for (int ks2 = 0; ks2 < 4; ++ks2) {
 #pragma unroll
-      for (int db = 0; db < D / 32; ++db) {
+      for (int db = 0; db < HD / 32; ++db) {
         const int dr = db * 32 + (lane & 31);
         const uint4 u = V[dr * 8 + ((ks2 * 2 + hl) ^ ((dr >> 1) & 7))];
         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, u), pf[ks2], o[db], 0, 0, 0);
       }
     }
-    sched_read_ahead<4 * D / 32, 4>();
+    sched_read_ahead<4 * HD / 32, 4>();
   };
-  // one pipeline step: tile j's scores are in s_cur
-  // (after the last tile the scores of a nonexistent tile j + 1 are computed
-  // from a stale buffer and discarded: no branch separates them from the softmax)
-  auto step = [&](int j, f32x16_t* s_cur, f32x16_t* s_nxt) {
-    // tile j + 1 resident for every wave; every wave is done with tile j - 1
+  f32x16_t sc_t[2];
+  for (int j = 0; j < ntiles; ++j) {
+    // tile j resident for every wave; every wave is done with tile j - 1
     wait_vmcnt0();
     __syncthreads();
     if (j + STAGES - 1 < ntiles) tile_load(j + STAGES - 1, (j + STAGES - 1) % STAGES);
-    scores((j + 1) % STAGES, s_nxt);
-    softmax_pv(j, j % STAGES, s_cur);
-  };
-  // without the score pipeline: tile j's scores, softmax and P V in turn
-  auto step_plain = [&](int j, f32x16_t* s_cur) {
-    wait_vmcnt0();
-    __syncthreads();
-    if (j + STAGES - 1 < ntiles) tile_load(j + STAGES - 1, (j + STAGES - 1) % STAGES);
-    scores(j % STAGES, s_cur);
-    softmax_pv(j, j % STAGES, s_cur);
-  };
-
-  f32x16_t sa[2], sb[2];
-  if constexpr (PIPE) {
-    wait_vmcnt0();
-    __syncthreads();
-    scores(0, sa);
-    for (int j = 0; j < ntiles; j += 2) {
-      step(j, sa, sb);
-      if (j + 1 < ntiles) step(j + 1, sb, sa);
-    }
-  } else {
-    for (int j = 0; j < ntiles; ++j) step_plain(j, sa);
+    scores(j % STAGES, sc_t);
+    softmax_pv(j, j % STAGES, sc_t);
   }
 
   const float l = l_i + __shfl_xor(l_i, 32, 64);
@@ -275,7 +249,7 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
     const int row = a.o_stream_major ? joint_to_row(a.meta, p) : p;
     bf16_t* og = (bf16_t*)a.o + (long)row * a.o_tok + (long)h * a.o_head;
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db)
+    for (int db = 0; db < HD / 32; ++db)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int dd = db * 32 + g * 8 + hl * 4;
@@ -384,26 +358,33 @@ AttnSched make_sched(const BatchMeta& m, int bq) {
 
 }  // namespace
 
-template <int NW, int STAGES, int PIPE>
+template <int NW, int HD>
 hipError_t launch_attn_cfg(const AttnArgs& a, hipStream_t s) {
   const AttnSched sc = make_sched(a.meta, NW * 32);
   const long blocks = (long)sc.tile_off[sc.n] * a.heads;
   if (blocks == 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_bf16_kernel<NW, STAGES, PIPE>), dim3((unsigned)blocks), dim3(NW * 64), 0, s, a, sc);
+  hipLaunchKernelGGL((attn_bf16_kernel<NW, HD, 2>), dim3((unsigned)blocks), dim3(NW * 64), 0, s, a, sc);
   return hipGetLastError();
 }
 
-// Measured on MI355X: the score pipeline (PIPE) needs 255 VGPRs and loses to
-// the plain order at 2 waves per SIMD, so the plain order with 2 buffers is used.
-hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s) {
-  if (a.head_dim != D) return hipErrorInvalidValue;
+// Measured on MI355X: a software pipeline that issues tile j + 1's score MFMAs
+// before tile j's softmax needs 255 VGPRs and loses to the plain order at 2
+// waves per SIMD, so the plain order with 2 buffers is used.
+template <int HD>
+hipError_t launch_attn_hd(const AttnArgs& a, hipStream_t s) {
   // Many blocks: 128 queries per block, two blocks per CU, so the two waves of
   // a SIMD belong to different blocks and drift apart (one in its softmax
   // while the other issues MFMAs); +10% at 16 896 tokens.  Fewer blocks: 256
   // queries per block, so the last round of blocks is fuller.
   const AttnSched sc4 = make_sched(a.meta, 4 * 32);
-  if ((long)sc4.tile_off[sc4.n] * a.heads >= 2048) return launch_attn_cfg<4, 2, 0>(a, s);
-  return launch_attn_cfg<8, 2, 0>(a, s);
+  if ((long)sc4.tile_off[sc4.n] * a.heads >= 2048) return launch_attn_cfg<4, HD>(a, s);
+  return launch_attn_cfg<8, HD>(a, s);
+}
+
+hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s) {
+  if (a.head_dim == 128) return launch_attn_hd<128>(a, s);
+  if (a.head_dim == 64) return launch_attn_hd<64>(a, s);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_attention_f32(const AttnArgs& a, hipStream_t s) {

@@ -112,8 +112,8 @@ dit_status check_config(const dit_config* c) {
     return fail(DIT_ERR_INVALID_ARG, "hidden %d != heads %d * head_dim %d", c->hidden, c->heads, c->head_dim);
   if (c->hidden % 64 != 0 || c->hidden > 4096)
     return fail(DIT_ERR_UNSUPPORTED, "hidden %d must be a multiple of 64 and <= 4096", c->hidden);
-  if (c->dtype == DIT_BF16 && c->head_dim != 128)
-    return fail(DIT_ERR_UNSUPPORTED, "bf16 models need head_dim 128 (got %d)", c->head_dim);
+  if (c->dtype == DIT_BF16 && c->head_dim != 128 && c->head_dim != 64)
+    return fail(DIT_ERR_UNSUPPORTED, "bf16 models need head_dim 128 or 64 (got %d)", c->head_dim);
   if (c->dtype == DIT_F32 && c->head_dim != 64)
     return fail(DIT_ERR_UNSUPPORTED, "fp32 models need head_dim 64 (got %d)", c->head_dim);
   if (c->mlp_ratio <= 0 || c->mlp_ratio > 8) return fail(DIT_ERR_INVALID_ARG, "mlp_ratio %d", c->mlp_ratio);
@@ -772,7 +772,7 @@ dit_status dit_attention(const dit_batch* batch, int heads, int head_dim, int dt
   if ((st = check_batch(batch, false))) return st;
   if (dtype != DIT_F32 && dtype != DIT_BF16) return fail(DIT_ERR_INVALID_ARG, "dtype %d", dtype);
   if (heads <= 0) return fail(DIT_ERR_INVALID_ARG, "heads %d", heads);
-  if ((dtype == DIT_BF16 && head_dim != 128) || (dtype == DIT_F32 && head_dim != 64))
+  if ((dtype == DIT_BF16 && head_dim != 128 && head_dim != 64) || (dtype == DIT_F32 && head_dim != 64))
     return fail(DIT_ERR_UNSUPPORTED, "head_dim %d with dtype %d", head_dim, dtype);
   if (!q || !k || !v || !o) return fail(DIT_ERR_INVALID_ARG, "q / k / v / o is NULL");
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o))

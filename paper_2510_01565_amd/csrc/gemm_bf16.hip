@@ -533,19 +533,59 @@ hipError_t launch_cfg(const GemmProblem& p, hipStream_t s) {
   return launch_kernel<BM, BN, NWM, NWN, BK, STAGES, false>(p, s);
 }
 
-enum GemmCfg { CFG_128x64 = 0, CFG_256x256 = 1, CFG_128x128 = 2 };
+enum GemmCfg { CFG_128x64 = 0, CFG_256x256 = 1, CFG_128x128 = 2, CFG_256x128 = 3, CFG_128x256 = 4 };
+
+// Launch-time model of the tile configurations, fitted to dit_linear timings
+// on MI355X over the step's GEMM shapes (M 768 .. 16896, N 1536 .. 21504,
+// K 1536 .. 15360): one CU works through ceil(tiles / 256) tiles one after
+// another, a tile costing its FLOPs at a per-CU rate plus a fixed prologue /
+// epilogue time.  Large tiles have the higher rate (fewer operand bytes per
+// FLOP); small tiles fill the 256 CUs when the big ones would leave most idle.
+struct TileModel {
+  GemmCfg cfg;
+  int bm, bn;
+  double tflops_per_cu;
+  double fixed_us;
+};
+constexpr TileModel kTileModels[] = {
+    {CFG_256x256, 256, 256, 7.31, 11.7},
+    {CFG_256x128, 256, 128, 6.11, 8.4},
+    {CFG_128x256, 128, 256, 6.23, 8.7},
+    {CFG_128x128, 128, 128, 5.07, 4.1},
+};
+
+double model_us(const TileModel& t, const GemmProblem& p) {
+  const long tn = (p.N + t.bn - 1) / t.bn;
+  long tiles = 0;
+  double work = 0.0;  // sum of tile times, microseconds
+  for (int g = 0; g < p.n_groups; ++g) {
+    const long tg = (long)((p.g[g].M + t.bm - 1) / t.bm) * tn;
+    tiles += tg;
+    work += tg * (2.0 * t.bm * t.bn * p.g[g].K / (t.tflops_per_cu * 1e6) + t.fixed_us);
+  }
+  if (tiles == 0) return 0.0;
+  return (double)((tiles + 255) / 256) * (work / tiles);
+}
+
 GemmCfg pick(const GemmProblem& p) {
-  int maxM = p.g[0].M;
-  if (p.n_groups > 1 && p.g[1].M > maxM) maxM = p.g[1].M;
   if (p.N <= 64) return CFG_128x64;
-  if (maxM >= 1024 && p.N >= 1024) return CFG_256x256;
-  return CFG_128x128;
+  GemmCfg best = CFG_128x128;
+  double best_us = 1e300;
+  for (const TileModel& t : kTileModels) {
+    const double us = model_us(t, p);
+    if (us < best_us) {
+      best_us = us;
+      best = t.cfg;
+    }
+  }
+  return best;
 }
 
 }  // namespace
 
 const char* gemm_bf16_config_name(const GemmProblem& p) {
-  static const char* names[] = {"gemm_bf16_128x64", "gemm_bf16_256x256", "gemm_bf16_128x128"};
+  static const char* names[] = {"gemm_bf16_128x64", "gemm_bf16_256x256", "gemm_bf16_128x128", "gemm_bf16_256x128",
+                                "gemm_bf16_128x256"};
   return names[pick(p)];
 }
 
@@ -555,6 +595,10 @@ hipError_t launch_gemm_bf16(const GemmProblem& p, hipStream_t s) {
       return launch_cfg<128, 64, 4, 1, 64, 2>(p, s);
     case CFG_256x256:
       return launch_cfg<256, 256, 4, 2, 64, 2>(p, s);
+    case CFG_256x128:
+      return launch_cfg<256, 128, 4, 2, 64, 2>(p, s);
+    case CFG_128x256:
+      return launch_cfg<128, 256, 2, 4, 64, 2>(p, s);
     default:
       return launch_cfg<128, 128, 2, 2, 64, 2>(p, s);
   }

@@ -4,7 +4,14 @@ Image tokens per request follow section 2.2, Table 1 of the paper
 (256 / 1024 / 4096 / 16384 tokens at 256 / 512 / 1024 / 2048 px, i.e.
 (resolution/16)^2, section 6.1).  The 57-block, 3072-wide, 24x128-head shape
 with 512 text tokens is the FLUX.1-dev class model the paper serves
-(section 6.1, "Models").
+(section 6.1, "Models").  The paper's second model, SD3 (section 6.1 and the
+4xA40 experiment of section 6.4), is served at the SD3-Medium shape: 24 joint
+blocks with separate weights for the text and image streams, 1536 wide,
+24x64 heads, 16 latent channels patchified 2x2 (64 input channels), 4096-wide
+text embeddings with 77 + 256 = 333 text tokens, 4096 image tokens at
+1024 px.  Only the shape is SD3's: the block is this library's adaLN joint
+block with 2-D RoPE (no learned position table, no pooled-text conditioning),
+and the weights are seeded random values.
 """
 from __future__ import annotations
 
@@ -54,6 +61,10 @@ FLUX_DOUBLE = ModelShape(hidden=3072, heads=24, head_dim=128, mlp_ratio=4, n_dou
                          in_channels=64, text_dim=4096)
 FLUX_FULL = ModelShape(hidden=3072, heads=24, head_dim=128, mlp_ratio=4, n_double=19, n_single=38,
                        in_channels=64, text_dim=4096)
+SD3_MEDIUM = ModelShape(hidden=1536, heads=24, head_dim=64, mlp_ratio=4, n_double=24, n_single=0,
+                        in_channels=64, text_dim=4096)
+SD3_DOUBLE = ModelShape(hidden=1536, heads=24, head_dim=64, mlp_ratio=4, n_double=1, n_single=0,
+                        in_channels=64, text_dim=4096)
 
 WORKLOADS = {
     "small_block_256px_f32": Workload(
@@ -92,6 +103,15 @@ WORKLOADS = {
     "dit57_512px_x4_bf16": Workload(
         "dit57_512px_x4_bf16", FLUX_FULL, [512] * 4, [512] * 4, t=None,
         note="4 identical 512 px requests batched in one step"),
+    "sd3m_1024px_bf16": Workload(
+        "sd3m_1024px_bf16", SD3_MEDIUM, [1024], [333], t=[0.5],
+        note="SD3-Medium shape: 24 joint blocks, 1536 wide, 24x64 heads, 333 text + 4096 image tokens, bf16"),
+    "sd3m_512px_bf16": Workload(
+        "sd3m_512px_bf16", SD3_MEDIUM, [512], [333], t=[0.5],
+        note="SD3-Medium shape: 24 joint blocks, 333 text + 1024 image tokens, bf16"),
+    "sd3m_packed_mixed_bf16": Workload(
+        "sd3m_packed_mixed_bf16", SD3_MEDIUM, [256, 512, 1024], [333, 333, 333], t=None,
+        note="SD3-Medium shape, 3 requests 256/512/1024 px packed, per-request timesteps U[0,1)"),
     "dit57_packed_mixed_bf16": Workload(
         "dit57_packed_mixed_bf16", FLUX_FULL, [256, 512, 1024, 2048], [512, 512, 512, 512], t=None,
         note="4 requests 256/512/1024/2048 px packed, per-request timesteps U[0,1)"),

@@ -72,8 +72,14 @@ def test_invalid_configs_are_rejected():
     cfg.heads = 23
     assert _err(dit.weight_count, cfg) == dit.DIT_ERR_INVALID_ARG
     cfg = dit.make_config(base)
-    cfg.head_dim, cfg.heads = 64, 48
+    cfg.head_dim, cfg.heads = 96, 32
     assert _err(dit.weight_count, cfg) == dit.DIT_ERR_UNSUPPORTED
+    cfg = dit.make_config(base)
+    cfg.head_dim, cfg.heads = 64, 48   # bf16 head_dim 64 (the SD3-Medium head) is supported
+    assert dit.weight_count(cfg) == dit.weight_count(dit.make_config(base))
+    f32 = dit.make_config(workloads.SMALL_BLOCK)
+    f32.head_dim, f32.heads = 128, 3   # fp32 attention is head_dim 64 only
+    assert _err(dit.weight_count, f32) == dit.DIT_ERR_UNSUPPORTED
     cfg = dit.make_config(base)
     cfg.in_channels = 12
     assert _err(dit.weight_count, cfg) == dit.DIT_ERR_UNSUPPORTED
@@ -121,7 +127,8 @@ def test_dit_step_validation_happens_before_any_launch():
     assert _err(dit.dit_block_forward, cfg, fake, 0, 1, b, P, P, P, need, 0) == dit.DIT_ERR_INVALID_ARG
     assert _err(dit.dit_block_forward, cfg, fake, 2, 0, b, P, P, P, need, 0) == dit.DIT_ERR_INVALID_ARG
     # attention head_dim unsupported for the dtype
-    assert _err(dit.dit_attention, b, 6, 64, dit.DIT_BF16, P, P, P, P, P, need, 0) == dit.DIT_ERR_UNSUPPORTED
+    assert _err(dit.dit_attention, b, 6, 96, dit.DIT_BF16, P, P, P, P, P, need, 0) == dit.DIT_ERR_UNSUPPORTED
+    assert _err(dit.dit_attention, b, 3, 128, dit.DIT_F32, P, P, P, P, P, need, 0) == dit.DIT_ERR_UNSUPPORTED
     # GEMM K not a multiple of 8
     assert _err(dit.dit_linear, 4, 4, 12, dit.DIT_BF16, P, P, 0, P, dit.DIT_F32, 0) == dit.DIT_ERR_UNSUPPORTED
     # Euler with a non-finite dt

@@ -53,11 +53,10 @@ def test_linear_real_shapes_sampled(M, N, K):
     assert normwise_err(got, ref) < F32_TOL
 
 
-def _attention_case(grids, n_txt, heads, seed, rows_per_req):
+def _attention_case(grids, n_txt, heads, seed, rows_per_req, d=128):
     torch = _torch()
     lens = [g * g + t for g, t in zip(grids, n_txt)]
     T = sum(lens)
-    d = 128
     q = _dev(seed, "q", (T, heads, d), 1.0, torch.bfloat16)
     k = _dev(seed, "k", (T, heads, d), 1.0, torch.bfloat16)
     v = _dev(seed, "v", (T, heads, d), 1.0, torch.bfloat16)
@@ -91,6 +90,20 @@ def test_attention_packed_mixed_sampled():
     lens = [g * g + 512 for g in grids]
     edge = [[0, L - 1, 511, 512, 255, 256] for L in lens]
     _attention_case(grids, [512] * 4, 24, 12, edge)
+
+
+def test_attention_sd3m_1024px_sampled():
+    """SD3-Medium shape at 1024 px: 24 heads of 64 over 333 text + 4096
+    image tokens (256-query blocks)."""
+    edge = [0, 332, 333, 334, 4428, 4427, 4415, 4416, 255, 256]
+    _attention_case([64], [333], 24, 13, [edge], d=64)
+
+
+def test_attention_sd3m_four_1024px_requests_sampled():
+    """Four packed SD3-Medium 1024 px requests (enough query tiles for the
+    128-query blocks), block-diagonal."""
+    edge = [0, 332, 333, 4428, 127, 128]
+    _attention_case([64] * 4, [333] * 4, 24, 14, [edge] * 4, d=64)
 
 
 def _block_weights(m, seed):
@@ -130,6 +143,32 @@ def test_double_block_1024px_sampled_rows():
                             (64, 64), rows_txt=rt, rows_img=ri)
     assert normwise_err(got[rt], ot) < BF16_TOL
     assert normwise_err(got[512 + ri], oi) < BF16_TOL
+
+
+def test_sd3m_joint_block_1024px_sampled_rows():
+    """SD3-Medium-shaped joint block at 1024 px (333 text + 4096 image
+    tokens, 1536 wide, 24x64 heads): sampled rows of both streams."""
+    torch = _torch()
+    m = workloads.SD3_DOUBLE
+    cfg, shapes, dev = _block_weights(m, 23)
+    H = m.hidden
+    x = _dev(23, "hidden", (333 + 4096, H), 1.0, torch.bfloat16).float()
+    c = _dev(23, "cond", (1, H), 1.0, torch.float32)
+    x_host = x.cpu().numpy().astype(np.float64)
+    b = dit.Batch([64], [64], [333], [0.5])
+    nws = dit.workspace_size(cfg, b)
+    ws = torch.empty(nws, dtype=torch.uint8, device="cuda")
+    dit.dit_block_forward(cfg, dit.Weights(dev), 0, 0, b, x, c, ws, nws)
+    torch.cuda.synchronize()
+    got = x.cpu().numpy()
+    params = _host_params(shapes, dev, ("double.0.", "mod."))
+    rng = np.random.default_rng(23)
+    rt = _rows(333, [0, 255, 256, 332], rng)
+    ri = _rows(4096, [0, 63, 64, 2047, 4095], rng)
+    ot, oi = O.double_block(params, oracle_cfg(m), 0, x_host[:333], x_host[333:], c.cpu().numpy()[0].astype(np.float64),
+                            (64, 64), rows_txt=rt, rows_img=ri)
+    assert normwise_err(got[rt], ot) < BF16_TOL
+    assert normwise_err(got[333 + ri], oi) < BF16_TOL
 
 
 def test_single_block_1024px_sampled_rows():

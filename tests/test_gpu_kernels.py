@@ -37,6 +37,35 @@ def test_linear_bf16(M, N, K, out):
         assert np.all(np.abs(g - ref) <= 2 ** -7 * np.abs(ref) + 1e-6 * np.abs(ref).max())
 
 
+@pytest.mark.parametrize("M,N,K,cfg", [
+    (5410, 659, 512, "256x128"), (5410, 659, 520, "256x128"),      # direct-to-LDS and register paths
+    (1303, 5429, 512, "128x256"), (1303, 5429, 520, "128x256"),
+    (5891, 1295, 512, "256x256"), (5891, 1295, 520, "256x256"),
+    (600, 500, 512, "128x128"), (600, 500, 520, "128x128"),
+])
+def test_linear_bf16_every_tile_config(M, N, K, cfg):
+    """Shapes for which the launch model picks each tile configuration (the
+    profile names the kernel that ran); 800 sampled outputs against fp64 dot
+    products, including the ragged last row and column."""
+    torch = _torch()
+    x = synth.normal(2, "x", (M, K), bf16=True)
+    w = synth.normal(2, "w", (N, K), std=0.02, bf16=True)
+    b = synth.normal(2, "b", (N,), std=0.02, bf16=True)
+    y = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    dit.profile_start()
+    dit.dit_linear(M, N, K, dit.DIT_BF16, to_dev(x, torch.bfloat16), to_dev(w, torch.bfloat16),
+                   to_dev(b, torch.bfloat16), y, dit.DIT_F32)
+    torch.cuda.synchronize()
+    ran = dit.profile_stop()
+    assert "gemm_bf16_" + cfg in ran, list(ran)
+    rng = np.random.default_rng(M * N + K)
+    ms = np.concatenate([[0, M - 1, M - 1, 127, 128], rng.integers(0, M, 795)])
+    ns = np.concatenate([[0, N - 1, 0, 255, 256], rng.integers(0, N, 795)])
+    ref = (x[ms].astype(np.float64) * w[ns].astype(np.float64)).sum(axis=1) + b[ns].astype(np.float64)
+    got = y.cpu().numpy()[ms, ns]
+    assert normwise_err(got, ref) < F32_TOL
+
+
 @pytest.mark.parametrize("M,N,K", [(5, 3, 8), (130, 70, 200), (300, 1152, 384)])
 def test_linear_f32(M, N, K):
     torch = _torch()
@@ -75,13 +104,14 @@ def _attn_case(grids, n_txt, heads, d, bf16, seed):
     return o.float().cpu().numpy(), ref
 
 
+@pytest.mark.parametrize("d", [128, 64])
 @pytest.mark.parametrize("grids,n_txt", [
     ([(16, 16)], [32]),                       # 288 tokens: 2 full + 1 partial query tile, ragged key tile
     ([(5, 7), (16, 16), (9, 13)], [3, 32, 17]),  # packed, lengths 38 / 288 / 134
     ([(1, 1)], [0]),                          # a single token
 ])
-def test_attention_bf16(grids, n_txt):
-    got, ref = _attn_case(grids, n_txt, 3, 128, True, 3)
+def test_attention_bf16(grids, n_txt, d):
+    got, ref = _attn_case(grids, n_txt, 3, d, True, 3)
     assert normwise_err(got, ref) < BF16_TOL
 
 
@@ -91,9 +121,10 @@ def test_attention_f32(grids, n_txt):
     assert normwise_err(got, ref) < F32_TOL
 
 
-def test_attention_identical_keys_give_mean_of_values():
+@pytest.mark.parametrize("d", [128, 64])
+def test_attention_identical_keys_give_mean_of_values(d):
     torch = _torch()
-    T, heads, d = 200, 2, 128
+    T, heads = 200, 2
     q = synth.normal(5, "q", (T, heads, d), bf16=True)
     k = np.broadcast_to(synth.normal(5, "k", (1, heads, d), bf16=True), (T, heads, d)).copy()
     v = synth.normal(5, "v", (T, heads, d), bf16=True)

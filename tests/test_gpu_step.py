@@ -16,6 +16,11 @@ TINY_BF16 = workloads.ModelShape(hidden=256, heads=2, head_dim=128, mlp_ratio=4,
                                  in_channels=64, text_dim=96)
 
 
+# the SD3-Medium block structure (joint blocks only, untied streams, 64-wide heads) at a small width
+TINY_SD3_BF16 = workloads.ModelShape(hidden=192, heads=3, head_dim=64, mlp_ratio=4, n_double=3, n_single=0,
+                                     in_channels=64, text_dim=80)
+
+
 def _run_step(m, params, shapes, cfg, grids, n_txt, ts, lat, txt):
     import torch
     dt = torch_dtype(m)
@@ -59,6 +64,18 @@ def test_tiny_bf16_packed_step():
     cfg, shapes, params = host_params(m, 1)
     grids, n_txt, ts = [(6, 10), (16, 16), (3, 4)], [17, 40, 0], [0.9, 0.25, 0.6]
     lat, txt = request_inputs(m, grids, n_txt, 1)
+    vel, _, _ = _run_step(m, params, shapes, cfg, grids, n_txt, ts, lat, txt)
+    ref = np.concatenate(_oracle_step(m, params, grids, n_txt, ts, lat, txt))
+    assert normwise_err(vel.float().cpu().numpy(), ref) < BF16_TOL
+
+
+def test_tiny_sd3_shaped_bf16_packed_step():
+    """Joint blocks only with 64-wide bf16 heads; three requests packed, one of
+    them without text."""
+    m = TINY_SD3_BF16
+    cfg, shapes, params = host_params(m, 4)
+    grids, n_txt, ts = [(8, 12), (16, 16), (5, 3)], [21, 77, 0], [0.3, 0.95, 0.05]
+    lat, txt = request_inputs(m, grids, n_txt, 4)
     vel, _, _ = _run_step(m, params, shapes, cfg, grids, n_txt, ts, lat, txt)
     ref = np.concatenate(_oracle_step(m, params, grids, n_txt, ts, lat, txt))
     assert normwise_err(vel.float().cpu().numpy(), ref) < BF16_TOL
