@@ -245,8 +245,7 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
   const float l = l_i + __shfl_xor(l_i, 32, 64);
   if (qrow < L) {
     const float inv = 1.0f / l;
-    const int p = a.meta.joint_off[r] + qrow;
-    const int row = a.o_stream_major ? joint_to_row(a.meta, p) : p;
+    const int row = a.o_stream_major ? padded_to_row(a.meta, r, qrow) : a.meta.joint_off[r] + qrow;
     bf16_t* og = (bf16_t*)a.o + (long)row * a.o_tok + (long)h * a.o_head;
 #pragma unroll
     for (int db = 0; db < HD / 32; ++db)
@@ -321,8 +320,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const AttnArgs a, const At
     }
   }
   if (qrow < L) {
-    const int p = a.meta.joint_off[r] + qrow;
-    const int row = a.o_stream_major ? joint_to_row(a.meta, p) : p;
+    const int row = a.o_stream_major ? padded_to_row(a.meta, r, qrow) : a.meta.joint_off[r] + qrow;
     float* og = (float*)a.o + (long)row * a.o_tok + (long)h * a.o_head;
     const float inv = 1.0f / l;
 #pragma unroll

@@ -14,7 +14,8 @@ constexpr int kMaxReq = DIT_MAX_REQUESTS;
 
 // Row bookkeeping of a packed batch.
 //  stream-major rows: [text of req 0 .. text of req n-1 | image of req 0 .. image of req n-1]
-//  joint positions:   [req 0: text, image | req 1: text, image | ...]  (attention order)
+//  joint positions:   [req 0: text, image | req 1: text, image | ...]  (the order of dit_attention)
+//  padded positions:  [req 0: image, text, pad | req 1: image, text, pad | ...]  (Q / K / V^T of the step)
 struct BatchMeta {
   int n_req;
   int T_txt;                 // total text rows
@@ -55,9 +56,23 @@ __host__ __device__ inline RowInfo row_info(const BatchMeta& m, int R) {
   return ri;
 }
 
-// position of a row inside the padded joint layout of Q, K and V^T
+// Position of a row inside the padded layout of Q, K and V^T that the step
+// uses: request r occupies [pad_off[r], pad_off[r + 1]) with its image tokens
+// first, then its text tokens.  Attention does not depend on the order of the
+// tokens inside a request; image-first starts both parts on a 16-token group
+// whenever the image count is a multiple of 16 (the (res/16)^2 grid of every
+// resolution that is a multiple of 64), so the QKV epilogue writes V^T in
+// whole 16-token groups whatever the text length.
+__host__ __device__ inline int req_images(const BatchMeta& m, int r) { return m.img_off[r + 1] - m.img_off[r]; }
+
 __host__ __device__ inline int padded_pos(const BatchMeta& m, const RowInfo& ri) {
-  return m.pad_off[ri.req] + (ri.is_img ? m.n_txt[ri.req] : 0) + ri.local;
+  return m.pad_off[ri.req] + (ri.is_img ? 0 : req_images(m, ri.req)) + ri.local;
+}
+
+// stream-major row of position q (0 <= q < L_r) of request r in that layout
+__host__ __device__ inline int padded_to_row(const BatchMeta& m, int r, int q) {
+  const int ni = req_images(m, r);
+  return q < ni ? m.T_txt + m.img_off[r] + q : m.txt_off[r] + (q - ni);
 }
 
 // Column of padded position `pos` in V^T.  Inside every aligned group of 16
@@ -65,14 +80,6 @@ __host__ __device__ inline int padded_pos(const BatchMeta& m, const RowInfo& ri)
 // which one 32x32 score fragment holds them; an involution.
 __host__ __device__ inline int vt_slot(int pos) { return (pos & ~12) | ((pos & 4) << 1) | ((pos & 8) >> 1); }
 
-// joint position -> stream-major row
-__host__ __device__ inline int joint_to_row(const BatchMeta& m, int p) {
-  int r = 0;
-  while (r + 1 < m.n_req && p >= m.joint_off[r + 1]) ++r;
-  int loc = p - m.joint_off[r];
-  if (loc < m.n_txt[r]) return m.txt_off[r] + loc;
-  return m.T_txt + m.img_off[r] + (loc - m.n_txt[r]);
-}
 
 // ----------------------------------------------------------------------------
 // GEMM epilogues: Y = A W^T + bias, then one of
@@ -133,8 +140,8 @@ hipError_t launch_gemm_f32(const GemmProblem& p, hipStream_t s);
 // name of the kernel configuration launch_gemm_bf16 picks for p
 const char* gemm_bf16_config_name(const GemmProblem& p);
 
-// Attention over the requests of a batch.  Token p of request r (joint
-// order, 0 <= p < L_r) is read from Q/K row qk_off[r] + p and from V^T
+// Attention over the requests of a batch.  Token p of request r
+// (0 <= p < L_r, in the order of o_stream_major) is read from Q/K row qk_off[r] + p and from V^T
 // column vt_off[r] + p; V^T columns of a request are padded to a multiple of
 // 64 (vt_off from pad_off) so that a 64-key tile never leaves the buffer.
 struct AttnArgs {
@@ -146,7 +153,8 @@ struct AttnArgs {
   long vt_head, vt_d;
   void* o;
   long o_tok, o_head;
-  int o_stream_major;   // 1: output row = joint_to_row(joint_off[r] + p); 0: joint_off[r] + p
+  int o_stream_major;   // 1: token p is padded position p of the step's layout, output row padded_to_row(r, p);
+                        // 0: token p is joint position p, output row joint_off[r] + p
   int heads;
   int head_dim;
   float scale;          // 1/sqrt(head_dim)

@@ -397,7 +397,7 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
     }
   }
 
-  // epilogue.  Row facts (request, joint position, grid position) are computed
+  // epilogue.  Row facts (request, padded position, grid position) are computed
   // once per tile row into LDS, so the unrolled loops never index the batch
   // metadata.  Each 32x32 accumulator fragment is staged through a per-wave
   // LDS buffer so that a lane ends up with 16 consecutive columns of one row
@@ -421,7 +421,7 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
     const int nl = nb + (lane & 31);
     const float bn = (bias != nullptr && nl < N) ? bf2f(bias[nl]) : 0.f;
     // V^T columns of a QKV epilogue: a lane takes one column and 16 consecutive
-    // rows, which (when they are 16 consecutive, 16-aligned joint positions of
+    // rows, which (when they are 16 consecutive, 16-aligned padded positions of
     // one request) land in one aligned 16-key group of V^T: two 16-byte stores.
     const bool vcols = E.mode == EPI_QKV && nb >= 2 * E.hidden && nb < 3 * E.hidden;
     static_for<FM>([&](auto ii) {
