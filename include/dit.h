@@ -82,7 +82,18 @@ typedef struct {
   float rope_theta;
   float ln_eps;
   int dtype;         /* dit_dtype */
+  int flags;         /* DIT_FLAG_* bits, 0 for the defaults */
 } dit_config;
+
+/*
+ * DIT_FLAG_BATCH_INVARIANT: every output bit of a request is independent of
+ * what it is packed with.  Without it, a bf16 GEMM launch with too few output
+ * tiles to fill the GPU may split its K range over several blocks whose fp32
+ * partial sums are added in a fixed order; results stay bitwise identical from
+ * run to run, but the order of the sums (and so the last bits) can change with
+ * the batch composition.  The flag also removes the split's workspace.
+ */
+#define DIT_FLAG_BATCH_INVARIANT 1
 
 /*
  * A packed batch of n_req requests (1..DIT_MAX_REQUESTS).  All arrays are

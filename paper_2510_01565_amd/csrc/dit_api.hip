@@ -127,6 +127,7 @@ dit_status check_config(const dit_config* c) {
     return fail(DIT_ERR_UNSUPPORTED, "time_freq_dim %d must be a positive multiple of 8", c->time_freq_dim);
   if (!(c->rope_theta > 0.f) || !(c->ln_eps > 0.f))
     return fail(DIT_ERR_INVALID_ARG, "rope_theta and ln_eps must be positive");
+  if (c->flags & ~DIT_FLAG_BATCH_INVARIANT) return fail(DIT_ERR_INVALID_ARG, "unknown flags 0x%x", c->flags);
   return DIT_OK;
 }
 
@@ -257,6 +258,8 @@ struct Workspace {
   void* K;       // [heads, Tp, d]
   void* Vt;      // [heads, d, Tp]
   void* Z;       // [T, H + F]  attention output | MLP hidden
+  float* sk_part;  // partial sums of split GEMMs (kSplitPartBytes), null when GEMMs never split
+  int* sk_cnt;     // their arrival counters [kSplitMaxTiles], zeroed at the start of every call
   size_t bytes;
 };
 
@@ -282,6 +285,9 @@ Workspace plan_workspace(const dit_config* c, const BatchMeta& m, char* base) {
   w.K = take((size_t)L.heads * Tp * L.d * es);
   w.Vt = take((size_t)L.heads * Tp * L.d * es);
   w.Z = take(T * (size_t)(L.H + L.F) * es);
+  const bool split = c->dtype == DIT_BF16 && !(c->flags & DIT_FLAG_BATCH_INVARIANT);
+  w.sk_part = split ? (float*)take(kSplitPartBytes) : nullptr;
+  w.sk_cnt = split ? (int*)take(kSplitMaxTiles * sizeof(int)) : nullptr;
   w.bytes = off;
   return w;
 }
@@ -409,6 +415,8 @@ GemmProblem problem(const Ctx& x, int N) {
   memset(&p, 0, sizeof(p));
   p.N = N;
   p.meta = x.meta;
+  p.sk_part = x.ws.sk_part;
+  p.sk_cnt = x.ws.sk_cnt;
   return p;
 }
 
@@ -652,6 +660,8 @@ dit_status dit_step(const dit_config* cfg, const dit_weights* w, const dit_batch
   // conditioning: c = W2 SiLU(W1 e(t) + b1) + b2; all modulation vectors m = Wm SiLU(c) + bm
   HIP_TRY(timed(x.s, "setup", 0.0, 0.0, [&] { return launch_rope_table(x.ws.rope, x.L.d, cfg->rope_theta, x.s); }));
   HIP_TRY(timed(x.s, "setup", 0.0, 0.0,
+                [&] { return launch_zero_i32(x.ws.sk_cnt, x.ws.sk_cnt ? kSplitMaxTiles : 0, x.s); }));
+  HIP_TRY(timed(x.s, "setup", 0.0, 0.0,
                 [&] { return launch_vt_pad_zero(dt, x.ws.Vt, meta, x.L.heads, x.L.d, x.s); }));
   HIP_TRY(timed(x.s, "setup", 0.0, 0.0,
                 [&] { return launch_timestep_embed(x.ws.temb, n, batch->t, cfg->time_freq_dim, x.s); }));
@@ -718,6 +728,8 @@ dit_status dit_block_forward(const dit_config* cfg, const dit_weights* w, int ki
   x.es = elem_size(cfg->dtype);
   const int H = x.L.H, n = meta.n_req;
   HIP_TRY(timed(x.s, "setup", 0.0, 0.0, [&] { return launch_rope_table(x.ws.rope, x.L.d, cfg->rope_theta, x.s); }));
+  HIP_TRY(timed(x.s, "setup", 0.0, 0.0,
+                [&] { return launch_zero_i32(x.ws.sk_cnt, x.ws.sk_cnt ? kSplitMaxTiles : 0, x.s); }));
   HIP_TRY(timed(x.s, "setup", 0.0, 0.0,
                 [&] { return launch_vt_pad_zero(cfg->dtype, x.ws.Vt, meta, x.L.heads, x.L.d, x.s); }));
   if (kind == 0) {

@@ -126,11 +126,21 @@ struct GemmGroup {
   EpiArgs epi;
 };
 
+// Split of K across blocks for launches with too few output tiles: every
+// tile's K range is cut into sk_p equal pieces run by sk_p blocks; each piece
+// publishes its fp32 partial sums, and the last piece of a tile to arrive adds
+// all of them in piece order and runs the epilogue.
+constexpr int kSplitMaxTiles = 1024;                   // arrival counters in the workspace
+constexpr long kSplitPartBytes = 96L * 1024 * 1024;    // partial-sum slots in the workspace
+
 struct GemmProblem {
   int N;
   int n_groups;  // 1 or 2
   GemmGroup g[2];
   BatchMeta meta;
+  float* sk_part;  // kSplitPartBytes of workspace, or null: never split
+  int* sk_cnt;     // kSplitMaxTiles arrival counters, zero before and after every launch
+  int sk_p;        // pieces per tile, set by the launcher (1: no split)
 };
 
 // ----------------------------------------------------------------------------
@@ -181,6 +191,8 @@ hipError_t launch_euler(int dtype, void* x, const void* v, int channels, const B
 // v [T_joint, heads, d] (joint order) -> vt [heads][d][pad_off[n]] at columns vt_slot(padded position)
 hipError_t launch_v_transpose(int dtype, const void* v, const BatchMeta& meta, int heads, int d, void* vt,
                               hipStream_t s);
+// n ints at p set to zero (a fill kernel, so a captured graph holds no memset node)
+hipError_t launch_zero_i32(int* p, int n, hipStream_t s);
 // zeroes the V^T columns of the padding keys of every request (padded positions >= the request length)
 hipError_t launch_vt_pad_zero(int dtype, void* vt, const BatchMeta& meta, int heads, int d, hipStream_t s);
 

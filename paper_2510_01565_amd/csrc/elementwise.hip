@@ -247,6 +247,19 @@ __global__ void vt_pad_zero_kernel(T* __restrict__ vt, const BatchMeta meta, lon
 
 }  // namespace
 
+namespace {
+__global__ void zero_i32_kernel(int* p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+}  // namespace
+
+hipError_t launch_zero_i32(int* p, int n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(zero_i32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, p, n);
+  return hipGetLastError();
+}
+
 hipError_t launch_vt_pad_zero(int dtype, void* vt, const BatchMeta& meta, int heads, int d, hipStream_t s) {
   const long ld = meta.pad_off[meta.n_req];
   const dim3 grid((unsigned)(heads * d));

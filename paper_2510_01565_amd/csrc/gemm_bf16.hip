@@ -16,6 +16,8 @@
 // operand panels those tiles share), in a grouped-M order.  One launch may
 // hold two problems ("groups") sharing N -- the text and image streams of a
 // double-stream block -- so the small text GEMM fills otherwise idle CUs.
+#include <string>
+
 #include "device_common.h"
 
 namespace dit {
@@ -28,11 +30,10 @@ struct TileCoord {
 };
 
 template <int BM, int BN>
-__device__ __forceinline__ TileCoord tile_coord(const GemmProblem& P) {
+__device__ __forceinline__ TileCoord tile_coord(const GemmProblem& P, int id) {
   const int tiles_n = (P.N + BN - 1) / BN;
   const int tm0 = (P.g[0].M + BM - 1) / BM;
   const int tiles0 = tm0 * tiles_n;
-  int id = xcd_remap(blockIdx.x, gridDim.x);
   int g = 0, tm = tm0;
   if (id >= tiles0) {
     g = 1;
@@ -88,7 +89,15 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
 
   __shared__ uint4 lds[STAGES * STAGE];
 
-  const TileCoord tc = tile_coord<BM, BN>(P);
+  // tile of this block and, when K is split, its piece; the pieces of a tile
+  // have consecutive indices and so run on one XCD
+  int tile_id = xcd_remap(blockIdx.x, gridDim.x), piece = 0;
+  const int np = DTL ? P.sk_p : 1;
+  if (np > 1) {
+    piece = tile_id % np;
+    tile_id /= np;
+  }
+  const TileCoord tc = tile_coord<BM, BN>(P, tile_id);
   const int gi = tc.group;
   const bf16_t* __restrict__ A = (const bf16_t*)(gi ? P.g[1].A : P.g[0].A);
   const bf16_t* __restrict__ W = (const bf16_t*)(gi ? P.g[1].W : P.g[0].W);
@@ -123,7 +132,10 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  const int KT = (K + BK - 1) / BK;
+  // K tiles [kb, kb + KT) of this block
+  const int KT_all = (K + BK - 1) / BK;
+  const int kb = piece * KT_all / np;
+  const int KT = (piece + 1) * KT_all / np - kb;
 
   // register path: fragments of k-step ks (16 wide) of stage st: lane row
   // (lane & 31), chunk 2 ks + lane / 32
@@ -246,7 +258,7 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
     char* const lbase = (char*)lds;
     // load instructions [q0, q1) of tile kt (A's first, then B's) into stage st
     auto load_part = [&](int st, int kt, int q0, int q1) __attribute__((always_inline)) {
-      const int koff = kt * BK * 2;
+      const int koff = (kb + kt) * BK * 2;
 #pragma unroll
       for (int q = 0; q < AI; ++q) {
         if (q < q0 || q >= q1) continue;
@@ -347,6 +359,64 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
     // the refetches of the last tile must land before the epilogue reuses LDS
     wait_vmcnt<0>();
     __syncthreads();
+
+    if (np > 1) {
+      // Split K: publish this piece's partial sums, or -- for the last piece
+      // of the tile to arrive -- add every piece's in piece order (the same
+      // order whichever piece arrives last) and go on to the epilogue.  A
+      // piece that finds all the others already counted skips publishing.
+      // Only thread 0 orders memory: the block barrier completes every wave's
+      // stores first, and only a block that reads the others' sums acquires
+      // (an acquire invalidates the L2 of its XCD, which blocks still
+      // multiplying there depend on).
+      constexpr int NV = AM * AN;
+      int* const flag = (int*)&lds[STAGES * STAGE - 1];  // past the epilogue's LDS (asserted below)
+      int* const cnt = P.sk_cnt + tile_id;
+      float4* const slots = (float4*)P.sk_part + (long)tile_id * np * NV * NT;
+      if (tid == 0) {
+        const bool last = __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == np - 1;
+        if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        *flag = last;
+      }
+      __syncthreads();
+      if (!*flag) {
+        float4* const mine = slots + (long)piece * NV * NT;
+#pragma unroll
+        for (int i = 0; i < AM; ++i)
+#pragma unroll
+          for (int j = 0; j < AN; ++j) {
+            const f32x4_t a4 = acc16[i][j];
+            mine[(i * AN + j) * NT + tid] = make_float4(a4[0], a4[1], a4[2], a4[3]);
+          }
+        __syncthreads();
+        if (tid == 0) {
+          const bool last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT) == np - 1;
+          if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+          *flag = last;
+        }
+        __syncthreads();
+        if (!*flag) return;  // uniform across the block
+      }
+#pragma unroll
+      for (int i = 0; i < AM; ++i)
+#pragma unroll
+        for (int j = 0; j < AN; ++j) {
+          f32x4_t t = {0.f, 0.f, 0.f, 0.f};
+          for (int qq = 0; qq < np; ++qq) {
+            if (qq == piece) {
+              t += acc16[i][j];
+            } else {
+              const float4 v = slots[((long)qq * NV + i * AN + j) * NT + tid];
+              t[0] += v.x;
+              t[1] += v.y;
+              t[2] += v.z;
+              t[3] += v.w;
+            }
+          }
+          acc16[i][j] = t;
+        }
+      if (tid == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
   } else {
     // ---- register path with zero-filled K tail (two LDS buffers).
     constexpr int A_CH = BM * CPR / NT, B_CH = BN * CPR / NT;
@@ -405,7 +475,7 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
   RowEntry* rows = (RowEntry*)&lds[0];
   constexpr int SP = 36;  // staging row pitch in floats (16-byte aligned rows)
   float* stg = (float*)&lds[0] + BM * (sizeof(RowEntry) / 4) + wave * 32 * SP;
-  static_assert(BM * sizeof(RowEntry) + NWAVES * 32 * SP * 4 <= sizeof(lds), "epilogue LDS");
+  static_assert(BM * sizeof(RowEntry) + NWAVES * 32 * SP * 4 <= sizeof(lds) - 16, "epilogue LDS (the last 16 bytes hold the split flag)");
   const EpiArgs E = gi ? P.g[1].epi : P.g[0].epi;
   const bool need_rows = E.mode == EPI_RESID || E.mode == EPI_QKV;
   if (need_rows) {
@@ -519,18 +589,20 @@ long tile_count(const GemmProblem& p) {
 }
 
 template <int BM, int BN, int NWM, int NWN, int BK, int STAGES, bool DTL>
-hipError_t launch_kernel(const GemmProblem& p, hipStream_t s) {
+hipError_t launch_kernel(const GemmProblem& p, int sk, hipStream_t s) {
   const long tiles = tile_count<BM, BN>(p);
   if (tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, NWM, NWN, BK, STAGES, DTL>), dim3((unsigned)tiles),
-                     dim3(NWM * NWN * 64), 0, s, p);
+  GemmProblem q = p;
+  q.sk_p = DTL ? sk : 1;
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, NWM, NWN, BK, STAGES, DTL>), dim3((unsigned)(tiles * q.sk_p)),
+                     dim3(NWM * NWN * 64), 0, s, q);
   return hipGetLastError();
 }
 
 template <int BM, int BN, int NWM, int NWN, int BK, int STAGES>
-hipError_t launch_cfg(const GemmProblem& p, hipStream_t s) {
-  if (dtl_ok<BM, BN, BK>(p)) return launch_kernel<BM, BN, NWM, NWN, BK, STAGES, true>(p, s);
-  return launch_kernel<BM, BN, NWM, NWN, BK, STAGES, false>(p, s);
+hipError_t launch_cfg(const GemmProblem& p, int sk, hipStream_t s) {
+  if (dtl_ok<BM, BN, BK>(p)) return launch_kernel<BM, BN, NWM, NWN, BK, STAGES, true>(p, sk, s);
+  return launch_kernel<BM, BN, NWM, NWN, BK, STAGES, false>(p, 1, s);
 }
 
 enum GemmCfg { CFG_128x64 = 0, CFG_256x256 = 1, CFG_128x128 = 2, CFG_256x128 = 3, CFG_128x256 = 4 };
@@ -553,54 +625,115 @@ constexpr TileModel kTileModels[] = {
     {CFG_128x256, 128, 256, 6.23, 8.7},
     {CFG_128x128, 128, 128, 5.07, 4.1},
 };
+// Split K: the merge adds, on the critical path, the write of a piece's
+// partial sums and the last piece's read of the others' (fp32, bm x bn per
+// piece) plus the arrival handshake.  A split is taken only when the model
+// predicts it saves at least kSplitMinGain of the launch.
+constexpr double kMergeFixedUs = 3.0;
+constexpr double kMergeBytesPerUs = 40e3;
+constexpr double kSplitMinGain = 0.10;
+constexpr int kSplitMaxPieces = 8;
 
-double model_us(const TileModel& t, const GemmProblem& p) {
+double model_us(const TileModel& t, const GemmProblem& p, int sk) {
   const long tn = (p.N + t.bn - 1) / t.bn;
   long tiles = 0;
-  double work = 0.0;  // sum of tile times, microseconds
+  double work = 0.0;  // sum of piece times, microseconds
   for (int g = 0; g < p.n_groups; ++g) {
     const long tg = (long)((p.g[g].M + t.bm - 1) / t.bm) * tn;
     tiles += tg;
-    work += tg * (2.0 * t.bm * t.bn * p.g[g].K / (t.tflops_per_cu * 1e6) + t.fixed_us);
+    work += tg * sk * (2.0 * t.bm * t.bn * p.g[g].K / sk / (t.tflops_per_cu * 1e6) + t.fixed_us);
   }
   if (tiles == 0) return 0.0;
-  return (double)((tiles + 255) / 256) * (work / tiles);
+  const long units = tiles * sk;
+  double us = (double)((units + 255) / 256) * (work / units);
+  if (sk > 1) us += kMergeFixedUs + (sk - 1) * 4.0 * t.bm * t.bn / kMergeBytesPerUs;
+  return us;
 }
 
-GemmCfg pick(const GemmProblem& p) {
-  if (p.N <= 64) return CFG_128x64;
-  GemmCfg best = CFG_128x128;
+bool dtl_for(GemmCfg c, const GemmProblem& p) {
+  switch (c) {
+    case CFG_256x256: return dtl_ok<256, 256, 64>(p);
+    case CFG_256x128: return dtl_ok<256, 128, 64>(p);
+    case CFG_128x256: return dtl_ok<128, 256, 64>(p);
+    case CFG_128x128: return dtl_ok<128, 128, 64>(p);
+    default: return false;
+  }
+}
+
+// K may be split when the caller gave split workspace, the direct-to-LDS path
+// runs, both groups share K, every piece keeps at least 4 K tiles, and the
+// counters and partial-sum slots suffice.
+bool split_ok(const TileModel& t, const GemmProblem& p, int sk) {
+  if (p.sk_part == nullptr || p.sk_cnt == nullptr || !dtl_for(t.cfg, p)) return false;
+  if (p.n_groups > 1 && p.g[0].K != p.g[1].K) return false;
+  if (p.g[0].K / 64 < 4 * sk) return false;
+  const long tn = (p.N + t.bn - 1) / t.bn;
+  long tiles = 0;
+  for (int g = 0; g < p.n_groups; ++g) tiles += (long)((p.g[g].M + t.bm - 1) / t.bm) * tn;
+  return tiles <= kSplitMaxTiles && tiles * sk * t.bm * t.bn * 4L <= kSplitPartBytes;
+}
+
+struct Choice {
+  GemmCfg cfg;
+  int sk;
+};
+
+Choice pick(const GemmProblem& p) {
+  if (p.N <= 64) return {CFG_128x64, 1};
+  Choice best{CFG_128x128, 1};
   double best_us = 1e300;
   for (const TileModel& t : kTileModels) {
-    const double us = model_us(t, p);
+    const double us = model_us(t, p, 1);
     if (us < best_us) {
       best_us = us;
-      best = t.cfg;
+      best = {t.cfg, 1};
     }
   }
-  return best;
+  Choice split = best;
+  double split_us = best_us;
+  for (const TileModel& t : kTileModels)
+    for (int sk = 2; sk <= kSplitMaxPieces; ++sk) {
+      if (!split_ok(t, p, sk)) continue;
+      const double us = model_us(t, p, sk);
+      if (us < split_us) {
+        split_us = us;
+        split = {t.cfg, sk};
+      }
+    }
+  return split_us <= (1.0 - kSplitMinGain) * best_us ? split : best;
 }
 
 }  // namespace
 
 const char* gemm_bf16_config_name(const GemmProblem& p) {
-  static const char* names[] = {"gemm_bf16_128x64", "gemm_bf16_256x256", "gemm_bf16_128x128", "gemm_bf16_256x128",
-                                "gemm_bf16_128x256"};
-  return names[pick(p)];
+  // "gemm_bf16_<tile>" and, for a split of K into k pieces, "..._k<k>"
+  struct Names {
+    std::string n[5][kSplitMaxPieces + 1];
+    Names() {
+      const char* base[] = {"gemm_bf16_128x64", "gemm_bf16_256x256", "gemm_bf16_128x128", "gemm_bf16_256x128",
+                            "gemm_bf16_128x256"};
+      for (int c = 0; c < 5; ++c)
+        for (int k = 0; k <= kSplitMaxPieces; ++k) n[c][k] = k <= 1 ? base[c] : base[c] + std::string("_k") + std::to_string(k);
+    }
+  };
+  static const Names names;
+  const Choice c = pick(p);
+  return names.n[c.cfg][c.sk].c_str();
 }
 
 hipError_t launch_gemm_bf16(const GemmProblem& p, hipStream_t s) {
-  switch (pick(p)) {
+  const Choice c = pick(p);
+  switch (c.cfg) {
     case CFG_128x64:
-      return launch_cfg<128, 64, 4, 1, 64, 2>(p, s);
+      return launch_cfg<128, 64, 4, 1, 64, 2>(p, 1, s);
     case CFG_256x256:
-      return launch_cfg<256, 256, 4, 2, 64, 2>(p, s);
+      return launch_cfg<256, 256, 4, 2, 64, 2>(p, c.sk, s);
     case CFG_256x128:
-      return launch_cfg<256, 128, 4, 2, 64, 2>(p, s);
+      return launch_cfg<256, 128, 4, 2, 64, 2>(p, c.sk, s);
     case CFG_128x256:
-      return launch_cfg<128, 256, 2, 4, 64, 2>(p, s);
+      return launch_cfg<128, 256, 2, 4, 64, 2>(p, c.sk, s);
     default:
-      return launch_cfg<128, 128, 2, 2, 64, 2>(p, s);
+      return launch_cfg<128, 128, 2, 2, 64, 2>(p, c.sk, s);
   }
 }
 

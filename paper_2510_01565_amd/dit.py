@@ -20,6 +20,7 @@ DIT_OK, DIT_ERR_INVALID_ARG, DIT_ERR_UNSUPPORTED, DIT_ERR_WORKSPACE, DIT_ERR_HIP
 DIT_F32, DIT_BF16 = 0, 1
 DIT_MAX_REQUESTS = 16
 DIT_MAX_GRID = 256
+DIT_FLAG_BATCH_INVARIANT = 1
 
 EXPORTED = ("dit_weight_count", "dit_weight_manifest", "dit_workspace_size", "dit_step", "dit_block_forward",
             "euler_update", "dit_attention_workspace_size", "dit_attention", "dit_linear", "dit_profile_start",
@@ -37,7 +38,7 @@ class dit_config(ctypes.Structure):
                 ("mlp_ratio", ctypes.c_int), ("n_double", ctypes.c_int), ("n_single", ctypes.c_int),
                 ("in_channels", ctypes.c_int), ("text_dim", ctypes.c_int), ("time_freq_dim", ctypes.c_int),
                 ("tie_streams", ctypes.c_int), ("rope_theta", ctypes.c_float), ("ln_eps", ctypes.c_float),
-                ("dtype", ctypes.c_int)]
+                ("dtype", ctypes.c_int), ("flags", ctypes.c_int)]
 
 
 class dit_batch(ctypes.Structure):
@@ -110,11 +111,12 @@ def _stream(s) -> Optional[int]:
     return s.cuda_stream
 
 
-def make_config(shape) -> dit_config:
-    """dit_config from a ``workloads.ModelShape``-like object."""
+def make_config(shape, flags: int = 0) -> dit_config:
+    """dit_config from a ``workloads.ModelShape``-like object; ``flags``: DIT_FLAG_* bits."""
     return dit_config(shape.hidden, shape.heads, shape.head_dim, shape.mlp_ratio, shape.n_double, shape.n_single,
                       shape.in_channels, shape.text_dim, shape.time_freq_dim, 1 if shape.tie_streams else 0,
-                      float(shape.rope_theta), float(shape.ln_eps), DIT_BF16 if shape.dtype == "bf16" else DIT_F32)
+                      float(shape.rope_theta), float(shape.ln_eps), DIT_BF16 if shape.dtype == "bf16" else DIT_F32,
+                      flags)
 
 
 class Batch:

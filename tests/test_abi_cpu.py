@@ -87,6 +87,21 @@ def test_invalid_configs_are_rejected():
     cfg.dtype = 7
     assert _err(dit.weight_count, cfg) == dit.DIT_ERR_INVALID_ARG
     assert "dtype" in dit.lib().dit_last_error().decode()
+    cfg = dit.make_config(base, 2)   # no such flag
+    assert _err(dit.weight_count, cfg) == dit.DIT_ERR_INVALID_ARG
+
+
+def test_split_workspace_only_without_batch_invariance():
+    """bf16 models reserve the split-K partial sums and counters unless
+    DIT_FLAG_BATCH_INVARIANT is set; fp32 models never do."""
+    b = dit.Batch([16], [16], [512], [0.5])
+    m = workloads.FLUX_FULL
+    free = dit.workspace_size(dit.make_config(m), b)
+    inv = dit.workspace_size(dit.make_config(m, dit.DIT_FLAG_BATCH_INVARIANT), b)
+    assert free - inv == 96 * 2 ** 20 + 4096
+    f32 = workloads.SMALL_BLOCK
+    assert dit.workspace_size(dit.make_config(f32), b) == \
+        dit.workspace_size(dit.make_config(f32, dit.DIT_FLAG_BATCH_INVARIANT), b)
 
 
 def test_invalid_batches_are_rejected():

@@ -106,9 +106,9 @@ def test_attention_sd3m_four_1024px_requests_sampled():
     _attention_case([64] * 4, [333] * 4, 24, 14, [edge] * 4, d=64)
 
 
-def _block_weights(m, seed):
+def _block_weights(m, seed, flags=0):
     torch = _torch()
-    cfg = dit.make_config(m)
+    cfg = dit.make_config(m, flags)
     shapes = dit.weight_manifest(cfg)
     dev = [synth.device_normal(seed, "w:" + n, s, synth.WEIGHT_STD, torch.bfloat16, torch.device("cuda"))
            for n, s in shapes]
@@ -196,6 +196,58 @@ def test_single_block_1024px_sampled_rows():
     assert normwise_err(got[rows], ref) < BF16_TOL
 
 
+@pytest.mark.parametrize("kind", [0, 1])
+def test_block_256px_split_k_sampled_rows(kind):
+    """A double (kind 0) or single (kind 1) FLUX-shaped block at 256 px (512
+    text + 256 image tokens): its GEMMs have too few tiles to fill the GPU, so
+    the launcher splits K (the profile names the split kernels).  Sampled rows
+    against the oracle; two runs agree bit for bit; the batch-invariant
+    configuration (no split) agrees within the bf16 tolerance."""
+    torch = _torch()
+    m = workloads.ModelShape(hidden=3072, heads=24, head_dim=128, mlp_ratio=4, n_double=1 - kind, n_single=kind,
+                             in_channels=64, text_dim=4096)
+    cfg, shapes, dev = _block_weights(m, 24 + kind)
+    H = m.hidden
+    x0 = _dev(24, "hidden", (512 + 256, H), 1.0, torch.bfloat16).float()
+    c = _dev(24, "cond", (1, H), 1.0, torch.float32)
+    b = dit.Batch([16], [16], [512], [0.5])
+
+    def run(cf, profile=False):
+        nws = dit.workspace_size(cf, b)
+        ws = torch.empty(nws, dtype=torch.uint8, device="cuda")
+        x = x0.clone()
+        if profile:
+            dit.profile_start()
+        dit.dit_block_forward(cf, dit.Weights(dev), kind, 0, b, x, c, ws, nws)
+        torch.cuda.synchronize()
+        ran = dit.profile_stop() if profile else None
+        return x, ran
+
+    got, ran = run(cfg, profile=True)
+    assert any(k.startswith("gemm_bf16_") and "_k" in k for k in ran), list(ran)
+    again, _ = run(cfg)
+    assert torch.equal(got, again)
+    inv, _ = run(dit.make_config(m, dit.DIT_FLAG_BATCH_INVARIANT))
+    x_host = x0.cpu().numpy().astype(np.float64)
+    got = got.cpu().numpy()
+    assert normwise_err(got - x_host, inv.cpu().numpy() - x_host) < BF16_TOL
+    rng = np.random.default_rng(24 + kind)
+    cc = c.cpu().numpy()[0].astype(np.float64)
+    if kind == 0:
+        params = _host_params(shapes, dev, ("double.0.", "mod."))
+        rt = _rows(512, [0, 255, 256, 511], rng)
+        ri = _rows(256, [0, 15, 16, 255], rng)
+        ot, oi = O.double_block(params, oracle_cfg(m), 0, x_host[:512], x_host[512:], cc, (16, 16), rows_txt=rt,
+                                rows_img=ri)
+        assert normwise_err(got[rt], ot) < BF16_TOL
+        assert normwise_err(got[512 + ri], oi) < BF16_TOL
+    else:
+        params = _host_params(shapes, dev, ("single.0.", "mod."))
+        rows = _rows(768, [0, 511, 512, 767], rng)
+        ref = O.single_block(params, oracle_cfg(m), 0, x_host, 512, cc, (16, 16), rows=rows)
+        assert normwise_err(got[rows], ref) < BF16_TOL
+
+
 def test_full_step_packed_equals_unpacked_and_deterministic():
     """The 57-block model on the packed 256/512/1024/2048 px batch (the
     benchmark's packed workload): the packed velocity equals each request
@@ -203,7 +255,8 @@ def test_full_step_packed_equals_unpacked_and_deterministic():
     torch = _torch()
     wl = workloads.WORKLOADS["dit57_packed_mixed_bf16"]
     m = wl.model
-    cfg, _, dev = _block_weights(m, 0)
+    # batch invariance is what DIT_FLAG_BATCH_INVARIANT promises (no split of K)
+    cfg, _, dev = _block_weights(m, 0, dit.DIT_FLAG_BATCH_INVARIANT)
     w = dit.Weights(dev)
     grids = wl.grids()
     ts = [float(t) for t in synth.uniform(0, "timesteps:" + wl.name, (4,))]

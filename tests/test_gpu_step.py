@@ -84,6 +84,7 @@ def test_tiny_sd3_shaped_bf16_packed_step():
 def test_packed_equals_unpacked_and_deterministic():
     m = TINY_BF16
     cfg, shapes, params = host_params(m, 2)
+    cfg = dit.make_config(m, dit.DIT_FLAG_BATCH_INVARIANT)
     grids, n_txt, ts = [(8, 8), (5, 9), (16, 12)], [33, 8, 64], [0.1, 0.5, 0.77]
     lat, txt = request_inputs(m, grids, n_txt, 2)
     packed, _, _ = _run_step(m, params, shapes, cfg, grids, n_txt, ts, lat, txt)
@@ -94,6 +95,28 @@ def test_packed_equals_unpacked_and_deterministic():
         one, _, _ = _run_step(m, params, shapes, cfg, [grids[r]], [n_txt[r]], [ts[r]], [lat[r]], [txt[r]])
         n = grids[r][0] * grids[r][1]
         assert bool((one == packed[off:off + n]).all()), r
+        off += n
+
+
+def test_sixteen_requests_and_extreme_grid_sides():
+    """The largest batch (16 requests) with the extreme grid shapes: a 1 x 256
+    and a 256 x 1 grid (RoPE positions up to the table's last row), single
+    tokens, no text, one text token, and requests whose lengths are not
+    multiples of 16; every request's velocity against the oracle."""
+    m = TINY_BF16
+    cfg, shapes, params = host_params(m, 5)
+    grids = [(1, 256), (256, 1), (1, 1), (1, 1), (2, 3), (7, 5), (16, 16), (3, 1), (1, 9), (12, 4), (5, 5), (9, 2),
+             (4, 4), (1, 2), (6, 6), (2, 17)]
+    n_txt = [0, 3, 0, 1, 77, 5, 0, 64, 2, 0, 31, 1, 16, 0, 9, 40]
+    ts = [float(t) for t in synth.uniform(5, "timesteps", (16,))]
+    lat, txt = request_inputs(m, grids, n_txt, 5)
+    vel, _, _ = _run_step(m, params, shapes, cfg, grids, n_txt, ts, lat, txt)
+    refs = _oracle_step(m, params, grids, n_txt, ts, lat, txt)
+    got = vel.float().cpu().numpy()
+    off = 0
+    for r, ref in enumerate(refs):
+        n = ref.shape[0]
+        assert normwise_err(got[off:off + n], ref) < BF16_TOL, r
         off += n
 
 
