@@ -123,8 +123,9 @@ dit_status check_config(const dit_config* c) {
     return fail(DIT_ERR_UNSUPPORTED, "in_channels %d must be a positive multiple of 8", c->in_channels);
   if (c->text_dim <= 0 || c->text_dim % 8 != 0)
     return fail(DIT_ERR_UNSUPPORTED, "text_dim %d must be a positive multiple of 8", c->text_dim);
-  if (c->time_freq_dim <= 0 || c->time_freq_dim % 8 != 0)
-    return fail(DIT_ERR_UNSUPPORTED, "time_freq_dim %d must be a positive multiple of 8", c->time_freq_dim);
+  if (c->time_freq_dim <= 0 || c->time_freq_dim % 8 != 0 || c->time_freq_dim > 4096)
+    return fail(DIT_ERR_UNSUPPORTED, "time_freq_dim %d must be a positive multiple of 8, at most 4096",
+                c->time_freq_dim);
   if (!(c->rope_theta > 0.f) || !(c->ln_eps > 0.f))
     return fail(DIT_ERR_INVALID_ARG, "rope_theta and ln_eps must be positive");
   if (c->flags & ~DIT_FLAG_BATCH_INVARIANT) return fail(DIT_ERR_INVALID_ARG, "unknown flags 0x%x", c->flags);
