@@ -40,9 +40,9 @@ __global__ void timestep_kernel(float* e, int n_req, TimeArgs ta, int dim) {
 // ---------------------------------------------------------------- GEMV
 // y[r, o] = sum_k W[o, k] act(x[r, k]) + b[o] for up to GV_R requests per
 // pass; activations staged in LDS, weights streamed once with 16-byte loads.
-// Each wavefront takes GV_V output rows at a time and requests all of their
-// chunks (a lane holds chunks lane, lane + 64, ... of each row) before any
-// arithmetic, so GV_V rows of loads are in flight per wave.  The weights are
+// Each wavefront takes GemvShape::V output rows at a time and requests all of
+// their chunks (a lane holds chunks lane, lane + 64, ... of each row) before
+// any arithmetic, so V rows of loads are in flight per wave.  The weights are
 // read once per step and never reused, so the loads are nontemporal (they do
 // not displace cached data); on MI355X this streams the 6.5 GB of the FLUX
 // modulation weights at about 6.8 TB/s against 5.5 TB/s for one row per wave
@@ -159,49 +159,53 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const float* __restrict__ X
   const float* mrow = mods + (long)ri.req * mods_ld;
   const float4* shv = (const float4*)(mrow + (ri.is_img ? sh_i : sh_t));
   const float4* scv = (const float4*)(mrow + (ri.is_img ? sc_i : sc_t));
-  float4 v[NV];
+  // float4 i of a lane is float4 lane + 64 i of the row; lanes past the row
+  // load its last float4 again and weigh it by zero (no load behind a branch,
+  // so all of them are in flight at once)
+  int cidx[NV];
+  float keep[NV];
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
-    const int c = lane + i * 64;
-    if (c < H4) {
-      v[i] = xr[c];
-    }
+    cidx[i] = min(lane + i * 64, H4 - 1);
+    keep[i] = lane + i * 64 < H4 ? 1.f : 0.f;
   }
+  float4 v[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) v[i] = xr[cidx[i]];
   float s = 0.f;
 #pragma unroll
-  for (int i = 0; i < NV; ++i)
-    if (lane + i * 64 < H4) s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
+  for (int i = 0; i < NV; ++i) s += keep[i] * ((v[i].x + v[i].y) + (v[i].z + v[i].w));
   const float mean = wave_sum(s) / (float)H;
   float ss = 0.f;
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
-    if (lane + i * 64 < H4) {
-      v[i].x -= mean;
-      v[i].y -= mean;
-      v[i].z -= mean;
-      v[i].w -= mean;
-      ss += (v[i].x * v[i].x + v[i].y * v[i].y) + (v[i].z * v[i].z + v[i].w * v[i].w);
-    }
+    v[i].x -= mean;
+    v[i].y -= mean;
+    v[i].z -= mean;
+    v[i].w -= mean;
+    ss += keep[i] * ((v[i].x * v[i].x + v[i].y * v[i].y) + (v[i].z * v[i].z + v[i].w * v[i].w));
   }
   const float rstd = 1.0f / sqrtf(wave_sum(ss) / (float)H + eps);
   OT* orow = out + (long)(R - row_begin) * ldo;
+  // Every lane stores: a lane past the row's end writes the row's last
+  // float4 with exactly the bytes the lane that owns it writes (same inputs,
+  // same arithmetic), so no store needs a branch and the shift / scale loads
+  // all leave before the first store.
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
-    const int c = lane + i * 64;
-    if (c < H4) {
-      const float4 sh = shv[c], sc = scv[c];
-      const float y0 = v[i].x * rstd * (1.f + sc.x) + sh.x;
-      const float y1 = v[i].y * rstd * (1.f + sc.y) + sh.y;
-      const float y2 = v[i].z * rstd * (1.f + sc.z) + sh.z;
-      const float y3 = v[i].w * rstd * (1.f + sc.w) + sh.w;
-      if constexpr (sizeof(OT) == 2) {
-        uint2 w;
-        w.x = pack_bf16x2(y0, y1);
-        w.y = pack_bf16x2(y2, y3);
-        *(uint2*)(orow + c * 4) = w;
-      } else {
-        *(float4*)(orow + c * 4) = make_float4(y0, y1, y2, y3);
-      }
+    const int c = cidx[i];
+    const float4 sh = shv[c], sc = scv[c];
+    const float y0 = v[i].x * rstd * (1.f + sc.x) + sh.x;
+    const float y1 = v[i].y * rstd * (1.f + sc.y) + sh.y;
+    const float y2 = v[i].z * rstd * (1.f + sc.z) + sh.z;
+    const float y3 = v[i].w * rstd * (1.f + sc.w) + sh.w;
+    if constexpr (sizeof(OT) == 2) {
+      uint2 w;
+      w.x = pack_bf16x2(y0, y1);
+      w.y = pack_bf16x2(y2, y3);
+      *(uint2*)(orow + c * 4) = w;
+    } else {
+      *(float4*)(orow + c * 4) = make_float4(y0, y1, y2, y3);
     }
   }
 }
