@@ -32,18 +32,18 @@ TEXT_TOKENS = 512
 XGMI_LINK_BYTES_PER_S = 153e9
 
 # full step on one GPU, ms
-STEP_MS_K1: Dict[int, float] = {256: 23.88, 512: 38.46, 1024: 76.18, 2048: 427.88}
+STEP_MS_K1: Dict[int, float] = {256: 15.98, 512: 25.41, 1024: 69.49, 2048: 391.76}
 # one GPU's share of a k-way split (compute only), ms
 SHARE_MS: Dict[int, Dict[int, float]] = {
-    256: {2: 21.44, 4: 20.99, 8: 20.77},
-    512: {2: 25.59, 4: 22.53, 8: 22.19},
-    1024: {2: 50.75, 4: 40.35, 8: 28.77},
-    2048: {2: 223.92, 4: 111.70, 8: 67.56},
+    256: {2: 13.3, 4: 12.44, 8: 11.93},
+    512: {2: 17.69, 4: 14.42, 8: 13.67},
+    1024: {2: 39.04, 4: 28.28, 8: 21.03},
+    2048: {2: 208.07, 4: 105.13, 8: 56.85},
 }
 # B identical requests in one step, ms per step (all B advance one step)
 BATCH_MS: Dict[int, Dict[int, float]] = {
-    256: {1: 23.88, 4: 54.16, 8: 109.02},
-    512: {1: 38.46, 2: 53.34, 4: 106.46},
+    256: {1: 15.98, 4: 44.75, 8: 87.25},
+    512: {1: 25.41, 2: 46.55, 4: 89.19},
 }
 
 
