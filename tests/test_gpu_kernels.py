@@ -115,6 +115,38 @@ def test_attention_bf16(grids, n_txt, d):
     assert normwise_err(got, ref) < BF16_TOL
 
 
+@pytest.mark.parametrize("d", [128, 64])
+@pytest.mark.parametrize("gain", [4.0, 16.0])
+def test_attention_bf16_large_logits(d, gain):
+    """Scores far outside the unit range: q and k scaled so that the log2-domain
+    logits reach tens (gain 4) or hundreds (gain 16), which takes the softmax
+    off its reference-0 path and through the rescales."""
+    torch = _torch()
+    grids, n_txt, heads = [(12, 12), (7, 9)], [40, 5], 2
+    lens = [gh * gw + nt for (gh, gw), nt in zip(grids, n_txt)]
+    T = sum(lens)
+    q = (synth.normal(6, "q", (T, heads, d)) * gain).astype(np.float32)
+    k = (synth.normal(6, "k", (T, heads, d)) * gain).astype(np.float32)
+    v = synth.normal(6, "v", (T, heads, d), bf16=True)
+    qb = torch.from_numpy(q).to(torch.bfloat16)
+    kb = torch.from_numpy(k).to(torch.bfloat16)
+    q64 = qb.float().numpy().astype(np.float64)
+    k64 = kb.float().numpy().astype(np.float64)
+    ref = np.empty((T, heads, d))
+    off = 0
+    for L in lens:
+        sl = slice(off, off + L)
+        ref[sl] = O.attention(q64[sl], k64[sl], v[sl].astype(np.float64))
+        off += L
+    b = dit.Batch([g[0] for g in grids], [g[1] for g in grids], n_txt)
+    wsb = dit.attention_workspace_size(b, heads, d, dit.DIT_BF16)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    o = torch.full((T, heads, d), float("nan"), dtype=torch.bfloat16, device="cuda")
+    dit.dit_attention(b, heads, d, dit.DIT_BF16, qb.cuda(), kb.cuda(), to_dev(v, torch.bfloat16), o, ws, wsb)
+    torch.cuda.synchronize()
+    assert normwise_err(o.float().cpu().numpy(), ref) < BF16_TOL
+
+
 @pytest.mark.parametrize("grids,n_txt", [([(16, 16)], [32]), ([(5, 7), (9, 13)], [3, 17])])
 def test_attention_f32(grids, n_txt):
     got, ref = _attn_case(grids, n_txt, 2, 64, False, 4)
