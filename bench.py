@@ -7,9 +7,11 @@ joint attention, gated MLP, gated residuals), the final layer and the
 flow-matching Euler update -- dit_step followed by euler_update.
 
 Default workload: the 1024 px request (4096 image + 512 text tokens) of the
-FLUX.1-dev-shaped model, bf16 weights with fp32 accumulation.  Weights and
-inputs are seeded random values drawn on the GPU (no trained checkpoint).
-Prints one JSON line on stdout; progress goes to stderr.
+FLUX.1-dev-shaped model, bf16 weights with fp32 accumulation; `value` is its
+steps/s.  The 256, 512 and 2048 px requests of the same model are timed too
+(per_workload).  Weights and inputs are seeded random values drawn on the GPU
+(no trained checkpoint).  Prints one JSON line on stdout; progress goes to
+stderr.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--extra A,B]
 """
@@ -305,9 +307,9 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="dit57_1024px_bf16")
-    ap.add_argument("--extra", default="",
-                    help="comma-separated further workloads to report per resolution, e.g. "
-                         "dit57_2048px_bf16,dit57_packed_mixed_bf16 (each also has its own default run)")
+    ap.add_argument("--extra", default="dit57_256px_bf16,dit57_512px_bf16,dit57_2048px_bf16",
+                    help="comma-separated further workloads reported per resolution under per_workload (default: "
+                         "the other resolutions of the paper's mix; '' for none)")
     ap.add_argument("--extra-steps", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -385,7 +387,12 @@ def main() -> int:
                    "text_tokens": wl.n_txt, "requests": len(g), "parallelism": "single GPU"},
         "tflops": main_res["tflops"], "frac_bf16_peak": main_res["frac_peak"],
         "tflop_per_step": main_res["tflop_per_step"], "cv_pct": main_res["cv_pct"],
-        "roofline": rl, "cpu_baseline": cpu, "per_workload": per, "scheduler": sched_lat,
+        "roofline": rl, "cpu_baseline": cpu,
+        "steps_per_s_by_resolution": {str(workloads.WORKLOADS[n].resolutions[0]): round(r["steps_per_s"], 3)
+                                      for n, r in per.items()
+                                      if workloads.WORKLOADS[n].model == wl.model and workloads.WORKLOADS[n].kind == "step"
+                                      and len(workloads.WORKLOADS[n].resolutions) == 1},
+        "per_workload": per, "scheduler": sched_lat,
         "kernels_ms_per_step": {k: round(v["ms_per_step"], 4) for k, v in main_res["kernels"].items()
                                 if not k.startswith("detail:")},
         "kernels": {k: {"launches_per_step": v["launches"] // max(1, min(args.steps, 3)), "avg_launch_ms": v["ms"] / v["launches"],
