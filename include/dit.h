@@ -174,6 +174,9 @@ dit_status euler_update(const dit_batch* batch, int channels, int dtype, void* l
  * request 1's, ...  q, k, v, o: [T_joint, heads, head_dim] of type dtype
  * (head h of token p at (p*heads + h)*head_dim).  This is the call a
  * sequence-parallel rank makes on the heads it owns after the all-to-all.
+ * head_dim: 128 or 64 for DIT_BF16 (bf16 operands, fp32 softmax state and
+ * accumulation, P rounded to bf16 for P V), 64 for DIT_F32 (all fp32);
+ * anything else returns DIT_ERR_UNSUPPORTED before any launch.
  * ws: at least dit_attention_workspace_size() bytes.
  */
 dit_status dit_attention_workspace_size(const dit_batch* batch, int heads, int head_dim, int dtype,
