@@ -370,12 +370,14 @@ hipError_t launch_attn_cfg(const AttnArgs& a, hipStream_t s) {
 // waves per SIMD, so the plain order with 2 buffers is used.
 template <int HD>
 hipError_t launch_attn_hd(const AttnArgs& a, hipStream_t s) {
-  // Many blocks: 128 queries per block, two blocks per CU, so the two waves of
-  // a SIMD belong to different blocks and drift apart (one in its softmax
-  // while the other issues MFMAs); +10% at 16 896 tokens.  Fewer blocks: 256
-  // queries per block, so the last round of blocks is fuller.
+  // 128 queries per block, two blocks per CU: the two waves of a SIMD belong
+  // to different blocks and drift apart (one in its softmax while the other
+  // issues MFMAs), measured on MI355X +10% at 16 896 tokens and +1.5% at
+  // 4 608 tokens over one block of 256 queries per CU.  At head dim 64 (half
+  // the registers, so two 256-query blocks fit on a CU) the 256-query blocks
+  // stay ahead until the launch has many blocks.
   const AttnSched sc4 = make_sched(a.meta, 4 * 32);
-  if ((long)sc4.tile_off[sc4.n] * a.heads >= 2048) return launch_attn_cfg<4, HD>(a, s);
+  if (HD == 128 || (long)sc4.tile_off[sc4.n] * a.heads >= 2048) return launch_attn_cfg<4, HD>(a, s);
   return launch_attn_cfg<8, HD>(a, s);
 }
 
