@@ -131,7 +131,12 @@ dit_status dit_weight_count(const dit_config* cfg, int* count);
  */
 dit_status dit_weight_manifest(const dit_config* cfg, int index, const char** name, int shape[2], int* ndim);
 
-/* Bytes of device workspace that dit_step / dit_block_forward need for this batch. */
+/*
+ * Bytes of device workspace that dit_step / dit_block_forward need for this
+ * batch: activations, Q / K / V^T, the modulation vectors and, for bf16
+ * models without DIT_FLAG_BATCH_INVARIANT, 96 MiB of split-K partial sums and
+ * 4 KiB of counters (zeroed by the calls themselves; no initialisation needed).
+ */
 dit_status dit_workspace_size(const dit_config* cfg, const dit_batch* batch, size_t* bytes);
 
 /*
