@@ -631,7 +631,7 @@ constexpr TileModel kTileModels[] = {
 // predicts it saves at least kSplitMinGain of the launch.
 constexpr double kMergeFixedUs = 3.0;
 constexpr double kMergeBytesPerUs = 40e3;
-constexpr double kSplitMinGain = 0.10;
+constexpr double kSplitMinGain = 0.05;
 constexpr int kSplitMaxPieces = 8;
 
 double model_us(const TileModel& t, const GemmProblem& p, int sk) {
