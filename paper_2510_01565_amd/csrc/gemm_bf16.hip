@@ -81,10 +81,13 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
   constexpr int NT = NWM * NWN * 64;
   constexpr int NWAVES = NWM * NWN;
   constexpr int WTM = BM / NWM, WTN = BN / NWN;
-  constexpr int FM = WTM / 32, FN = WTN / 32;
+  // wave tiles: rows in 32-row fragments; columns in 32-column fragments on
+  // the register path, in 16-column fragments on the direct-to-LDS path
+  constexpr int FM = WTM / 32, FN = WTN / 32, FN16 = WTN / 16;
   constexpr int CPR = BK / 8;                     // 16-byte chunks per tile row
   constexpr int STAGE = (BM + BN) * CPR;          // uint4 per stage
-  static_assert(FM >= 1 && FN >= 1 && (BK == 32 || BK == 64) && STAGES >= 2 && BK % 32 == 0, "tile config");
+  static_assert(FM * 32 == WTM && FN16 * 16 == WTN && (DTL || FN * 32 == WTN), "wave tile");
+  static_assert(FM >= 1 && FN16 >= 1 && (BK == 32 || BK == 64) && STAGES >= 2 && BK % 32 == 0, "tile config");
   static_assert(STAGES * STAGE * 16 <= 160 * 1024, "LDS");
 
   __shared__ uint4 lds[STAGES * STAGE];
@@ -115,7 +118,7 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
 
   // Accumulators.  Direct-to-LDS path: 16x16 blocks, the 32x32 fragment
   // (i, j) being the 2 x 2 blocks 2i.., 2j..; register path: 32x32 blocks.
-  constexpr int AM = DTL ? 2 * FM : 1, AN = DTL ? 2 * FN : 1;
+  constexpr int AM = DTL ? 2 * FM : 1, AN = DTL ? FN16 : 1;
   constexpr int CM = DTL ? 1 : FM, CN = DTL ? 1 : FN;
   f32x4_t acc16[AM][AN];
   f32x16_t acc[CM][CN];
@@ -215,7 +218,7 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
     constexpr int ROWB = CPR * 16;                      // bytes per LDS row
     constexpr int A_STAGE = BM * ROWB, B_STAGE = BN * ROWB;
     constexpr int B_REGION = STAGES * A_STAGE;
-    constexpr int FM2 = 2 * FM, FN2 = 2 * FN;           // 16-row fragments per wave tile
+    constexpr int FM2 = 2 * FM, FN2 = FN16;             // 16-row / 16-column fragments per wave tile
     constexpr int NR2 = FM2 + FN2;                      // fragment reads per k-step
     constexpr int NMP = FM * FN2;                       // MFMAs per phase
     static_assert(B_REGION + STAGES * B_STAGE <= (int)sizeof(lds), "LDS");
@@ -485,8 +488,13 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
   }
   const bf16_t* bias = (const bf16_t*)E.bias;
   const int rl = lane >> 1, cseg = (lane & 1) * 16;
-  static_for<FN>([&](auto jj) {
+  // column groups of 32 (the last one 16 wide when the wave tile is an odd
+  // number of 16-column fragments)
+  constexpr int NJ = DTL ? (FN16 + 1) / 2 : FN;
+  static_for<NJ>([&](auto jj) {
     constexpr int j = decltype(jj)::value;
+    constexpr int NB16 = DTL ? (FN16 - 2 * j < 2 ? FN16 - 2 * j : 2) : 2;  // 16-column blocks in the group
+    constexpr int NCOL = 16 * NB16;
     const int nb = n0 + wn * WTN + j * 32;
     const int nl = nb + (lane & 31);
     const float bn = (bias != nullptr && nl < N) ? bf2f(bias[nl]) : 0.f;
@@ -497,7 +505,7 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
     static_for<FM>([&](auto ii) {
       constexpr int i = decltype(ii)::value;
       if constexpr (DTL) {
-        static_for<2>([&](auto bb) {
+        static_for<NB16>([&](auto bb) {
           constexpr int b = decltype(bb)::value;
           const int nl16 = nb + b * 16 + (lane & 15);
           const float bn16 = (bias != nullptr && nl16 < N) ? bf2f(bias[nl16]) : 0.f;
@@ -522,7 +530,7 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
         for (int q = 0; q < 16; ++q) v[q] = stg[(rh * 16 + q) * SP + c];
         const int ml0 = wm * WTM + i * 32 + rh * 16;
         const int m = m0 + ml0, n = nb + c;
-        if (n < N && m < M) {
+        if (c < NCOL && n < N && m < M) {
           const RowEntry r0 = rows[ml0];
           const bool whole = m + 15 < M && (r0.pos & 15) == 0 && rows[ml0 + 15].pos == r0.pos + 15;
           const int hn = n - 2 * E.hidden, h = hn / E.head_dim, dd = hn - h * E.head_dim;
@@ -552,7 +560,7 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
       });
       const int ml = wm * WTM + i * 32 + rl;
       const int m = m0 + ml, n = nb + cseg;
-      if (m < M) {
+      if (cseg < NCOL && m < M) {
         RowEntry re;
         if (need_rows) re = rows[ml];
         if (n + 16 <= N) {
@@ -605,7 +613,15 @@ hipError_t launch_cfg(const GemmProblem& p, int sk, hipStream_t s) {
   return launch_kernel<BM, BN, NWM, NWN, BK, STAGES, false>(p, 1, s);
 }
 
-enum GemmCfg { CFG_128x64 = 0, CFG_256x256 = 1, CFG_128x128 = 2, CFG_256x128 = 3, CFG_128x256 = 4 };
+// direct-to-LDS-only configurations (wave tiles of an odd number of 16-column
+// fragments have no register path): the 256x256 register path otherwise
+template <int BM, int BN, int NWM, int NWN, int BK, int STAGES>
+hipError_t launch_cfg_dtl_only(const GemmProblem& p, int sk, hipStream_t s) {
+  if (dtl_ok<BM, BN, BK>(p)) return launch_kernel<BM, BN, NWM, NWN, BK, STAGES, true>(p, sk, s);
+  return launch_cfg<256, 256, 4, 2, 64, 2>(p, 1, s);
+}
+
+enum GemmCfg { CFG_128x64 = 0, CFG_256x256 = 1, CFG_128x128 = 2, CFG_256x128 = 3, CFG_128x256 = 4, CFG_288x192 = 5 };
 
 // Launch-time model of the tile configurations, fitted to dit_linear timings
 // on MI355X over the step's GEMM shapes (M 768 .. 16896, N 1536 .. 21504,
@@ -619,11 +635,16 @@ struct TileModel {
   double tflops_per_cu;
   double fixed_us;
 };
+// 288x192 (12 waves of 96x48) divides 4608 x 3072 into exactly 256 tiles;
+// its rate is set from the same large shapes on which 256x256 was measured
+// (0.915 of 256x256's when both fill the GPU).  It is considered only for
+// launches it covers in one round (see pick).
 constexpr TileModel kTileModels[] = {
     {CFG_256x256, 256, 256, 7.31, 11.7},
     {CFG_256x128, 256, 128, 6.11, 8.4},
     {CFG_128x256, 128, 256, 6.23, 8.7},
     {CFG_128x128, 128, 128, 5.07, 4.1},
+    {CFG_288x192, 288, 192, 6.31, 8.0},
 };
 // Split K: the merge adds, on the critical path, the write of a piece's
 // partial sums and the last piece's read of the others' (fp32, bm x bn per
@@ -656,6 +677,7 @@ bool dtl_for(GemmCfg c, const GemmProblem& p) {
     case CFG_256x128: return dtl_ok<256, 128, 64>(p);
     case CFG_128x256: return dtl_ok<128, 256, 64>(p);
     case CFG_128x128: return dtl_ok<128, 128, 64>(p);
+    case CFG_288x192: return dtl_ok<288, 192, 64>(p);
     default: return false;
   }
 }
@@ -683,6 +705,14 @@ Choice pick(const GemmProblem& p) {
   Choice best{CFG_128x128, 1};
   double best_us = 1e300;
   for (const TileModel& t : kTileModels) {
+    // 288x192 has no register path, and it measured faster inside the step
+    // only where its tiles fit in one round and the epilogue is not the
+    // residual update (its 48-column wave tiles leave half the lanes idle in
+    // every other epilogue segment, which the residual's read-modify-write of
+    // x makes expensive)
+    if (t.cfg == CFG_288x192 && (!dtl_for(t.cfg, p) || tile_count<288, 192>(p) > 256 ||
+                                 p.g[0].epi.mode == EPI_RESID))
+      continue;
     const double us = model_us(t, p, 1);
     if (us < best_us) {
       best_us = us;
@@ -693,7 +723,7 @@ Choice pick(const GemmProblem& p) {
   double split_us = best_us;
   for (const TileModel& t : kTileModels)
     for (int sk = 2; sk <= kSplitMaxPieces; ++sk) {
-      if (!split_ok(t, p, sk)) continue;
+      if (t.cfg == CFG_288x192 || !split_ok(t, p, sk)) continue;  // 288x192: one-round launches only
       const double us = model_us(t, p, sk);
       if (us < split_us) {
         split_us = us;
@@ -708,11 +738,11 @@ Choice pick(const GemmProblem& p) {
 const char* gemm_bf16_config_name(const GemmProblem& p) {
   // "gemm_bf16_<tile>" and, for a split of K into k pieces, "..._k<k>"
   struct Names {
-    std::string n[5][kSplitMaxPieces + 1];
+    std::string n[6][kSplitMaxPieces + 1];
     Names() {
       const char* base[] = {"gemm_bf16_128x64", "gemm_bf16_256x256", "gemm_bf16_128x128", "gemm_bf16_256x128",
-                            "gemm_bf16_128x256"};
-      for (int c = 0; c < 5; ++c)
+                            "gemm_bf16_128x256", "gemm_bf16_288x192"};
+      for (int c = 0; c < 6; ++c)
         for (int k = 0; k <= kSplitMaxPieces; ++k) n[c][k] = k <= 1 ? base[c] : base[c] + std::string("_k") + std::to_string(k);
     }
   };
@@ -732,6 +762,8 @@ hipError_t launch_gemm_bf16(const GemmProblem& p, hipStream_t s) {
       return launch_cfg<256, 128, 4, 2, 64, 2>(p, c.sk, s);
     case CFG_128x256:
       return launch_cfg<128, 256, 2, 4, 64, 2>(p, c.sk, s);
+    case CFG_288x192:
+      return launch_cfg_dtl_only<288, 192, 3, 4, 64, 2>(p, c.sk, s);
     default:
       return launch_cfg<128, 128, 2, 2, 64, 2>(p, c.sk, s);
   }

@@ -40,7 +40,8 @@ def test_linear_bf16(M, N, K, out):
 @pytest.mark.parametrize("M,N,K,cfg", [
     (5410, 659, 512, "256x128"), (5410, 659, 520, "256x128"),      # direct-to-LDS and register paths
     (1303, 5429, 512, "128x256"), (1303, 5429, 520, "128x256"),
-    (5891, 1295, 512, "256x256"), (5891, 1295, 520, "256x256"),
+    (6001, 2313, 512, "256x256"), (6001, 2313, 520, "256x256"),
+    (5891, 1295, 512, "288x192"),                                  # direct-to-LDS only (96x48 wave tiles)
     (600, 500, 512, "128x128"), (600, 500, 520, "128x128"),
 ])
 def test_linear_bf16_every_tile_config(M, N, K, cfg):
