@@ -549,6 +549,38 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
         }
         return;
       }
+      if constexpr (NCOL == 16) {
+        if (E.mode == EPI_RESID) {
+          // a 16-wide group under the residual update: 8 columns per lane so
+          // that every lane of the wave reads, updates and writes x
+          const int c8 = (lane & 1) * 8;
+          const int ml = wm * WTM + i * 32 + rl;
+          const int m = m0 + ml, n = nb + c8;
+          if (m < M) {
+            const RowEntry re = rows[ml];
+            const float* g = E.mods + (long)re.req * E.mods_ld + E.gate_off + n;
+            float* xo = (float*)E.out + (long)m * E.ldo + n;
+            if (n + 8 <= N) {
+#pragma unroll
+              for (int q = 0; q < 2; ++q) {
+                const float4 t = *(const float4*)&stg[rl * SP + c8 + 4 * q];
+                const float4 gv = ((const float4*)g)[q];
+                float4 xv = ((float4*)xo)[q];
+                xv.x += gv.x * t.x;
+                xv.y += gv.y * t.y;
+                xv.z += gv.z * t.z;
+                xv.w += gv.w * t.w;
+                ((float4*)xo)[q] = xv;
+              }
+            } else {
+#pragma unroll
+              for (int q = 0; q < 8; ++q)
+                if (n + q < N) xo[q] += g[q] * stg[rl * SP + c8 + q];
+            }
+          }
+          return;
+        }
+      }
       float v[16];
       static_for<4>([&](auto qq) {
         constexpr int q = decltype(qq)::value;
@@ -706,13 +738,8 @@ Choice pick(const GemmProblem& p) {
   double best_us = 1e300;
   for (const TileModel& t : kTileModels) {
     // 288x192 has no register path, and it measured faster inside the step
-    // only where its tiles fit in one round and the epilogue is not the
-    // residual update (its 48-column wave tiles leave half the lanes idle in
-    // every other epilogue segment, which the residual's read-modify-write of
-    // x makes expensive)
-    if (t.cfg == CFG_288x192 && (!dtl_for(t.cfg, p) || tile_count<288, 192>(p) > 256 ||
-                                 p.g[0].epi.mode == EPI_RESID))
-      continue;
+    // only where its tiles fit in one round
+    if (t.cfg == CFG_288x192 && (!dtl_for(t.cfg, p) || tile_count<288, 192>(p) > 256)) continue;
     const double us = model_us(t, p, 1);
     if (us < best_us) {
       best_us = us;
