@@ -242,23 +242,43 @@ def scheduler_latency(seed: int):
             "allocate_us_28_steps": round((time.perf_counter() - t0) / 200 * 1e6, 2)}
 
 
+def kernel_of(family: str) -> str:
+    """Kernel a profiler family belongs to: the bf16 GEMM's tile configurations
+    and K splits ("gemm_bf16_256x256", "gemm_bf16_128x256_k3", ...) are launch
+    parameters of one kernel, "gemm_bf16"; other families are their own kernel."""
+    return "gemm_bf16" if family.startswith("gemm_bf16_") else family
+
+
 def roofline(kernels, dtype: str, workload: str):
-    """Dominant kernel family by time: algorithmic work per launch over its
-    average launch duration (HIP events on the launch stream)."""
-    name, k = max(((n, v) for n, v in kernels.items() if not n.startswith("detail:")), key=lambda kv: kv[1]["ms"])
+    """Dominant kernel by time: algorithmic work per launch over its average
+    launch duration (HIP events on the launch stream), with the measured HBM
+    bytes per launch when every family of the kernel has a current counter
+    summary."""
+    agg = {}
+    for n, v in kernels.items():
+        if n.startswith("detail:"):
+            continue
+        a = agg.setdefault(kernel_of(n), {"ms": 0.0, "launches": 0, "flops": 0.0, "bytes": 0.0, "families": {}})
+        for f in ("ms", "launches", "flops", "bytes"):
+            a[f] += v[f]
+        a["families"][n] = v["launches"]
+    name, k = max(agg.items(), key=lambda kv: kv[1]["ms"])
     avg_ms = k["ms"] / k["launches"]
-    traffic = measured_traffic(name, workload)
+    per_family = {f: measured_traffic(f, workload) for f in k["families"]}
+    traffic = None
+    if all(t is not None for t in per_family.values()):
+        traffic = sum(per_family[f] * n for f, n in k["families"].items()) / k["launches"]
+    common = {"kernel": name, "families": {f: n for f, n in k["families"].items()}, "traffic": traffic,
+              "avg_launch_ms": avg_ms, "algorithmic_bytes_per_launch": k["bytes"] / k["launches"],
+              "launches": k["launches"]}
     if k["flops"] > 0:
         peak = BF16_PEAK_TFLOPS if dtype == "bf16" else F32_PEAK_TFLOPS
         ach = k["flops"] / k["launches"] / (avg_ms / 1e3) / 1e12
-        return {"kernel": name, "bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s",
-                "frac": ach / peak, "traffic": traffic, "avg_launch_ms": avg_ms,
-                "flop_per_launch": k["flops"] / k["launches"], "algorithmic_bytes_per_launch": k["bytes"] / k["launches"],
-                "launches": k["launches"]}
+        return {"bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s", "frac": ach / peak,
+                "flop_per_launch": k["flops"] / k["launches"], **common}
     ach = k["bytes"] / k["launches"] / (avg_ms / 1e3) / 1e9
-    return {"kernel": name, "bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": ach / HBM_PEAK_GBS, "traffic": traffic, "avg_launch_ms": avg_ms,
-            "algorithmic_bytes_per_launch": k["bytes"] / k["launches"], "launches": k["launches"]}
+    return {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS,
+            **common}
 
 
 def cpu_baseline(wl, seed: int):
