@@ -77,7 +77,7 @@ typedef struct {
   int n_single;
   int in_channels;   /* C_in of the patchified latents, a multiple of 8 */
   int text_dim;      /* width of the text embeddings, a multiple of 8 */
-  int time_freq_dim; /* width of the sinusoidal timestep embedding (even) */
+  int time_freq_dim; /* width of the sinusoidal timestep embedding, a multiple of 8, at most 4096 */
   int tie_streams;
   float rope_theta;
   float ln_eps;
