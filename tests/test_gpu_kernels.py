@@ -110,6 +110,8 @@ def _attn_case(grids, n_txt, heads, d, bf16, seed):
     ([(16, 16)], [32]),                       # 288 tokens: 2 full + 1 partial query tile, ragged key tile
     ([(5, 7), (16, 16), (9, 13)], [3, 32, 17]),  # packed, lengths 38 / 288 / 134
     ([(1, 1)], [0]),                          # a single token
+    ([(8, 8)], [0]),                          # exactly one 64-key tile
+    ([(8, 8), (11, 11)], [1, 7]),             # 65 and 128 tokens: one key past a tile, exactly two tiles
 ])
 def test_attention_bf16(grids, n_txt, d):
     got, ref = _attn_case(grids, n_txt, 3, d, True, 3)

@@ -69,6 +69,17 @@ def test_tiny_bf16_packed_step():
     assert normwise_err(vel.float().cpu().numpy(), ref) < BF16_TOL
 
 
+def test_text_free_batch_step():
+    """A batch with no text tokens at all (no text embedder rows, text_emb NULL)."""
+    m = TINY_BF16
+    cfg, shapes, params = host_params(m, 6)
+    grids, n_txt, ts = [(8, 8), (4, 12)], [0, 0], [0.4, 0.8]
+    lat, txt = request_inputs(m, grids, n_txt, 6)
+    vel, _, _ = _run_step(m, params, shapes, cfg, grids, n_txt, ts, lat, txt)
+    ref = np.concatenate(_oracle_step(m, params, grids, n_txt, ts, lat, txt))
+    assert normwise_err(vel.float().cpu().numpy(), ref) < BF16_TOL
+
+
 def test_tiny_sd3_shaped_bf16_packed_step():
     """Joint blocks only with 64-wide bf16 heads; three requests packed, one of
     them without text."""
