@@ -16,7 +16,8 @@ def _torch():
     return torch
 
 
-@pytest.mark.parametrize("M,N,K", [(77, 64, 40), (300, 200, 136), (2500, 1100, 520), (513, 3072, 3072)])
+@pytest.mark.parametrize("M,N,K", [(1, 1, 8), (1, 3001, 64), (77, 64, 40), (300, 200, 136), (2500, 1100, 520),
+                                   (513, 3072, 3072)])
 @pytest.mark.parametrize("out", ["f32", "bf16"])
 def test_linear_bf16(M, N, K, out):
     torch = _torch()
