@@ -329,6 +329,14 @@ const char* epi_name(int mode) {
 
 hipError_t gemm(hipStream_t s, int dtype, const GemmProblem& p) {
   const int es = dtype == DIT_BF16 ? 2 : 4;
+  if (dtype == DIT_BF16 && gemm_bf16_split_groups(p)) {
+    GemmProblem q = p;
+    q.n_groups = 1;
+    const hipError_t e = gemm(s, dtype, q);
+    if (e != hipSuccess) return e;
+    q.g[0] = p.g[1];
+    return gemm(s, dtype, q);
+  }
   if (dtype == DIT_BF16) {
     if (!prof().on)
       return launch_gemm_bf16(p, s);

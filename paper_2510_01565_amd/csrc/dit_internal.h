@@ -149,6 +149,9 @@ hipError_t launch_gemm_bf16(const GemmProblem& p, hipStream_t s);
 hipError_t launch_gemm_f32(const GemmProblem& p, hipStream_t s);
 // name of the kernel configuration launch_gemm_bf16 picks for p
 const char* gemm_bf16_config_name(const GemmProblem& p);
+// whether the launch model predicts p's two groups to finish sooner as two
+// launches of one group each (the caller then launches them in turn)
+bool gemm_bf16_split_groups(const GemmProblem& p);
 
 // Attention over the requests of a batch.  Token p of request r
 // (0 <= p < L_r, in the order of o_stream_major) is read from Q/K row qk_off[r] + p and from V^T

@@ -732,7 +732,11 @@ struct Choice {
   int sk;
 };
 
-Choice pick(const GemmProblem& p) {
+// pick(): the configuration and K split with the shortest modelled launch
+// (its time, in microseconds, in *us when asked for; 0 for the skinny-N path,
+// which the model does not cover)
+Choice pick(const GemmProblem& p, double* us_out = nullptr) {
+  if (us_out) *us_out = 0.0;
   if (p.N <= 64) return {CFG_128x64, 1};
   Choice best{CFG_128x128, 1};
   double best_us = 1e300;
@@ -757,10 +761,33 @@ Choice pick(const GemmProblem& p) {
         split = {t.cfg, sk};
       }
     }
-  return split_us <= (1.0 - kSplitMinGain) * best_us ? split : best;
+  const bool take_split = split_us <= (1.0 - kSplitMinGain) * best_us;
+  if (us_out) *us_out = take_split ? split_us : best_us;
+  return take_split ? split : best;
 }
 
+// Two groups as two launches: the image group of a double block often fills
+// whole rounds of 256x256 tiles by itself (4096 rows x 12288 at 1024 px,
+// 16384 x 3072 at 2048 px), and the text group's few tiles then open a last
+// round that is mostly idle.  Run alone, the text group takes a tiling of its
+// own (smaller tiles, split K) and finishes in a fraction of a round.  The
+// second launch costs one kernel boundary.
+constexpr double kLaunchGapUs = 4.0;
+constexpr double kGroupSplitMinGain = 0.03;
+
 }  // namespace
+
+bool gemm_bf16_split_groups(const GemmProblem& p) {
+  if (p.n_groups < 2 || p.N <= 64) return false;
+  double both = 0.0, first = 0.0, second = 0.0;
+  pick(p, &both);
+  GemmProblem q = p;
+  q.n_groups = 1;
+  pick(q, &first);
+  q.g[0] = p.g[1];
+  pick(q, &second);
+  return first + second + kLaunchGapUs <= (1.0 - kGroupSplitMinGain) * both;
+}
 
 const char* gemm_bf16_config_name(const GemmProblem& p) {
   // "gemm_bf16_<tile>" and, for a split of K into k pieces, "..._k<k>"
