@@ -20,6 +20,7 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import re
 import statistics
 import sys
 import time
@@ -134,11 +135,15 @@ def measured_traffic(family: str, workload: str):
     """HBM bytes per launch from the committed counter summary
     profiles/hbm_traffic.txt (FETCH_SIZE and WRITE_SIZE passes, each scaled by
     the same counter's reading for a plain copy of known size), or None when
-    no summary exists for this kernel, workload and kernel source."""
+    no summary exists for this kernel, workload and kernel source.  The
+    counters see kernels, not K splits: a family "<tile>_k<n>" takes the
+    reading of its tile configuration's kernel, which is averaged over all of
+    that kernel's launches in the workload, split or not."""
     path = os.path.join(ROOT, "profiles", "hbm_traffic.txt")
     if not os.path.exists(path):
         return None
     want = kernel_source_hash(family)
+    family = re.sub(r"_k\d+$", "", family)
     for line in open(path):
         f = line.split()
         if len(f) >= 4 and not line.startswith("#") and f[0] == family and f[1] == workload and f[2] == want:

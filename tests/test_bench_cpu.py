@@ -60,3 +60,15 @@ def test_more_than_one_gpu_is_refused():
                        text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_split_family_takes_its_kernels_traffic(tmp_path, monkeypatch):
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    h = bench.kernel_source_hash("gemm_bf16_128x128")
+    (prof / "hbm_traffic.txt").write_text(f"# header\ngemm_bf16_128x128 wl {h} 1.5e+08 1e+08 5e+07 4\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda fam: h)
+    assert bench.measured_traffic("gemm_bf16_128x128_k2", "wl") == pytest.approx(1.5e8)
+    assert bench.measured_traffic("gemm_bf16_128x128", "wl") == pytest.approx(1.5e8)
+    assert bench.measured_traffic("gemm_bf16_128x256_k2", "wl") is None
