@@ -210,6 +210,49 @@ def run_sp_share(torch, dit, synth, workloads, wl, cfg, w, steps, seed, dev):
                     f"launches of {heads} heads over {L} tokens (HIP events); all-to-alls excluded"}
 
 
+def block_flops(m, n_txt, n_img) -> dict:
+    """Algorithmic FLOPs of one double-stream block: its GEMMs (QKV, output
+    projection, MLP up and down on every token), its modulation GEMV from the
+    conditioning vector, and attention inside each request."""
+    H, F = m.hidden, m.mlp_ratio * m.hidden
+    T = sum(n_txt) + sum(n_img)
+    streams = 1 if m.tie_streams else 2
+    g = 2.0 * T * H * (3 * H + H + F + F) + 2.0 * len(n_img) * streams * 6 * H * H
+    a = sum(4.0 * (lt + li) ** 2 * m.head_dim * m.heads for lt, li in zip(n_txt, n_img))
+    return {"gemm": g, "attention": a, "total": g + a}
+
+
+def run_block(torch, dit, synth, wl, cfg, w, steps, seed, dev):
+    """One double-stream block through dit_block_forward (fp32 residual in
+    place, bf16 weights), timed with HIP events on the launch stream."""
+    m = wl.model
+    grids = wl.grids()
+    n_img = wl.n_img()
+    b = dit.Batch(grids, grids, wl.n_txt, [0.5] * len(grids))
+    nws = dit.workspace_size(cfg, b)
+    ws = torch.empty(nws, dtype=torch.uint8, device=dev)
+    hidden = synth.device_normal(seed, "hidden:" + wl.name, (sum(wl.n_txt) + sum(n_img), m.hidden), 1.0,
+                                 torch.float32, dev)
+    cond = synth.device_normal(seed, "cond:" + wl.name, (len(grids), m.hidden), 1.0, torch.float32, dev)
+    stream = torch.cuda.current_stream()
+    for _ in range(2):
+        dit.dit_block_forward(cfg, w, 0, 0, b, hidden, cond, ws, nws, stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(steps):
+        dit.dit_block_forward(cfg, w, 0, 0, b, hidden, cond, ws, nws, stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    assert torch.isfinite(hidden).all().item(), "non-finite block output"
+    ms = e0.elapsed_time(e1) / steps
+    f = block_flops(m, wl.n_txt, n_img)
+    tf = f["total"] / (ms / 1e3) / 1e12
+    del ws, hidden, cond
+    return {"ms_per_block": ms, "gflop_per_block": f["total"] / 1e9, "tflops": tf,
+            "frac_peak": tf / (BF16_PEAK_TFLOPS if m.dtype == "bf16" else F32_PEAK_TFLOPS)}
+
+
 def scheduler_latency(seed: int):
     """Decision latency of the round scheduler (host C++): one ts_round_schedule
     call over R pending requests of the paper's resolution mix on N = 8 GPUs,
@@ -382,6 +425,12 @@ def main() -> int:
         if ow.kind == "attention_share":
             r = run_sp_share(torch, dit, synth, workloads, ow, cfg, w, args.extra_steps, args.seed, dev)
             log(f"{name}: {r['ms_per_step']:.2f} ms per share step, {r['tflops']:.1f} TFLOP/s ({r['note']})")
+            per[name] = r
+            continue
+        if ow.kind == "double_block":
+            r = run_block(torch, dit, synth, ow, cfg, w, max(args.extra_steps, 10), args.seed, dev)
+            log(f"{name}: {r['ms_per_block'] * 1e3:.1f} us per block, {r['tflops']:.1f} TFLOP/s "
+                f"({100 * r['frac_peak']:.1f}% of peak)")
             per[name] = r
             continue
         if ow.kind != "step":

@@ -72,3 +72,15 @@ def test_split_family_takes_its_kernels_traffic(tmp_path, monkeypatch):
     assert bench.measured_traffic("gemm_bf16_128x128_k2", "wl") == pytest.approx(1.5e8)
     assert bench.measured_traffic("gemm_bf16_128x128", "wl") == pytest.approx(1.5e8)
     assert bench.measured_traffic("gemm_bf16_128x256_k2", "wl") is None
+
+
+def test_double_block_flops_match_the_c2_count():
+    # one FLUX double block at 512 text + 1024 image tokens: 347.9 GFLOP of
+    # GEMM (2 T H (3H + H + 2F)), 29.0 of attention (4 L^2 d heads), plus the
+    # block's modulation GEMV (2 streams x 6H x H)
+    from paper_2510_01565_amd import workloads
+    m = workloads.FLUX_DOUBLE
+    f = bench.block_flops(m, [512], [1024])
+    assert f["attention"] == pytest.approx(4.0 * 1536 ** 2 * 128 * 24)
+    assert f["gemm"] == pytest.approx(2.0 * 1536 * 3072 * 36864 + 2.0 * 2 * 6 * 3072 * 3072)
+    assert f["total"] / 1e9 == pytest.approx(377.1, abs=0.1)
