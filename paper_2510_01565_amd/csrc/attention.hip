@@ -262,13 +262,17 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
 
 // ----------------------------------------------------------------------------
 // fp32 attention (head_dim 64) for fp32 models: one thread per query, K and V
-// tiles of 64 keys in LDS, online softmax in fp32 with expf.
+// tiles of 64 keys in LDS (rows of 16 float4, padded to 17 so the tile stores
+// of a wave spread over the banks; the compute reads are broadcasts), and the
+// online softmax taken per tile in fp32 with expf: all 64 scores of a tile
+// (independent dot products), one rescale of O and l, then O += P V.
 constexpr int FD = 64;
 constexpr int FQ = 64;
 
 __global__ __launch_bounds__(64) void attn_f32_kernel(const AttnArgs a, const AttnSched sc) {
-  __shared__ float Ksh[64][FD + 1];
-  __shared__ float Vsh[64][FD + 1];
+  constexpr int F4 = FD / 4;
+  __shared__ float4 Ksh[64][F4 + 1];
+  __shared__ float4 Vsh[64][F4 + 1];
   const int per_head = sc.tile_off[sc.n];
   const int h = blockIdx.x / per_head;
   const int t = blockIdx.x - h * per_head;
@@ -284,39 +288,83 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const AttnArgs a, const At
   const float* Kg = (const float*)a.k + (long)a.qk_off[r] * a.k_tok + (long)h * a.k_head;
   const float* Vg = (const float*)a.vt + (long)a.vt_off[r] + (long)h * a.vt_head;
 
-  float q[FD], o[FD];
+  float4 q[F4], o[F4];
 #pragma unroll
-  for (int c = 0; c < FD; ++c) {
-    q[c] = (qrow < L) ? Qg[(long)qrow * a.q_tok + c] : 0.f;
-    o[c] = 0.f;
+  for (int c = 0; c < F4; ++c) {
+    q[c] = (qrow < L) ? *(const float4*)(Qg + (long)qrow * a.q_tok + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
+    o[c] = make_float4(0.f, 0.f, 0.f, 0.f);
   }
   float m = -INFINITY, l = 0.f;
   for (int kv0 = 0; kv0 < L; kv0 += 64) {
     __syncthreads();
-    for (int idx = tid; idx < 64 * FD; idx += 64) {
-      const int kr = idx / FD, c = idx % FD;
-      const bool ok = kv0 + kr < L;
-      Ksh[kr][c] = ok ? Kg[(long)(kv0 + kr) * a.k_tok + c] : 0.f;
-    }
-    for (int idx = tid; idx < 64 * FD; idx += 64) {
-      const int c = idx / 64, kr = idx % 64;
-      const bool ok = kv0 + kr < L;
-      Vsh[kr][c] = ok ? Vg[(long)c * a.vt_d + vt_slot(kv0 + kr)] : 0.f;
+    // Each operand's tile arrives as 16 float4 loads per thread, all in flight
+    // before the LDS stores.  K rows past L re-read row L - 1 (their scores are
+    // masked); V^T is read in slot order, 64 slots of the request's padded
+    // columns per d, and slot s holds key vt_slot(s) (an involution).
+    {
+      float4 tq[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int idx = tid + u * 64;
+        tq[u] = *(const float4*)(Kg + (long)min(kv0 + (idx >> 4), L - 1) * a.k_tok + (idx & 15) * 4);
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int idx = tid + u * 64;
+        Ksh[idx >> 4][idx & 15] = tq[u];
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int idx = tid + u * 64;
+        tq[u] = *(const float4*)(Vg + (long)(idx >> 4) * a.vt_d + kv0 + (idx & 15) * 4);
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int idx = tid + u * 64, c = idx >> 4, s0 = kv0 + (idx & 15) * 4;
+        ((float*)Vsh[vt_slot(s0) - kv0])[c] = tq[u].x;
+        ((float*)Vsh[vt_slot(s0 + 1) - kv0])[c] = tq[u].y;
+        ((float*)Vsh[vt_slot(s0 + 2) - kv0])[c] = tq[u].z;
+        ((float*)Vsh[vt_slot(s0 + 3) - kv0])[c] = tq[u].w;
+      }
     }
     __syncthreads();
     const int nk = min(64, L - kv0);
-    for (int j = 0; j < nk; ++j) {
-      float sdot = 0.f;
+    float s[64];
+    float mx = m;
 #pragma unroll
-      for (int c = 0; c < FD; ++c) sdot = fmaf(q[c], Ksh[j][c], sdot);
-      const float sc_ = sdot * a.scale;
-      const float mn = fmaxf(m, sc_);
-      const float al = expf(m - mn);
-      const float p = expf(sc_ - mn);
-      l = l * al + p;
+    for (int j = 0; j < 64; ++j) {
+      float d0 = 0.f, d1 = 0.f;
 #pragma unroll
-      for (int c = 0; c < FD; ++c) o[c] = fmaf(p, Vsh[j][c], o[c] * al);
-      m = mn;
+      for (int c = 0; c < F4; c += 2) {
+        const float4 k0 = Ksh[j][c], k1 = Ksh[j][c + 1];
+        d0 = fmaf(q[c].x, k0.x, fmaf(q[c].y, k0.y, fmaf(q[c].z, k0.z, fmaf(q[c].w, k0.w, d0))));
+        d1 = fmaf(q[c + 1].x, k1.x, fmaf(q[c + 1].y, k1.y, fmaf(q[c + 1].z, k1.z, fmaf(q[c + 1].w, k1.w, d1))));
+      }
+      s[j] = j < nk ? (d0 + d1) * a.scale : -INFINITY;
+      mx = fmaxf(mx, s[j]);
+    }
+    // mx is finite: the tile holds at least one key
+    const float al = expf(m - mx);
+    float ps = 0.f;
+#pragma unroll
+    for (int j = 0; j < 64; ++j) {
+      s[j] = expf(s[j] - mx);
+      ps += s[j];
+    }
+    l = l * al + ps;
+    m = mx;
+#pragma unroll
+    for (int c = 0; c < F4; ++c) {
+      float4 acc = make_float4(o[c].x * al, o[c].y * al, o[c].z * al, o[c].w * al);
+#pragma unroll
+      for (int j = 0; j < 64; ++j) {
+        const float4 v = Vsh[j][c];
+        acc.x = fmaf(s[j], v.x, acc.x);
+        acc.y = fmaf(s[j], v.y, acc.y);
+        acc.z = fmaf(s[j], v.z, acc.z);
+        acc.w = fmaf(s[j], v.w, acc.w);
+      }
+      o[c] = acc;
     }
   }
   if (qrow < L) {
@@ -324,7 +372,8 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const AttnArgs a, const At
     float* og = (float*)a.o + (long)row * a.o_tok + (long)h * a.o_head;
     const float inv = 1.0f / l;
 #pragma unroll
-    for (int c = 0; c < FD; ++c) og[c] = o[c] * inv;
+    for (int c = 0; c < F4; ++c)
+      *(float4*)(og + 4 * c) = make_float4(o[c].x * inv, o[c].y * inv, o[c].z * inv, o[c].w * inv);
   }
 }
 

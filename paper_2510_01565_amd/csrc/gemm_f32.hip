@@ -35,18 +35,35 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmProblem P) {
   const int tx = tid & 15, ty = tid >> 4;  // 16 x 16 threads, each 4 x 4 outputs
   float acc[4][4] = {};
 
-  for (int k0 = 0; k0 < K; k0 += TK) {
-    // 64 rows x 16 k per operand = 1024 values, 4 per thread
+  // 64 rows x 16 k per operand = 1024 values, 4 per thread.  The next K tile
+  // is loaded into registers while this one is multiplied; addresses are
+  // clamped into the operands (no load behind a branch, so all of them are in
+  // flight at once) and values outside them replaced by zero.
+  float ra[4], rb[4];
+  auto gload = [&](int k0) {
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       const int idx = tid + c * 256;
       const int row = idx >> 4, kk = idx & 15;
       const int gk = k0 + kk;
-      const int ra = m0 + row, rb = n0 + row;
-      As[kk][row] = (ra < M && gk < K) ? A[(long)ra * lda + gk] : 0.f;
-      Bs[kk][row] = (rb < N && gk < K) ? W[(long)rb * ldw + gk] : 0.f;
+      const int am = m0 + row, bn = n0 + row;
+      const float va = A[(long)min(am, M - 1) * lda + min(gk, K - 1)];
+      const float vb = W[(long)min(bn, N - 1) * ldw + min(gk, K - 1)];
+      ra[c] = (am < M && gk < K) ? va : 0.f;
+      rb[c] = (bn < N && gk < K) ? vb : 0.f;
+    }
+  };
+  gload(0);
+  for (int k0 = 0; k0 < K; k0 += TK) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int idx = tid + c * 256;
+      const int row = idx >> 4, kk = idx & 15;
+      As[kk][row] = ra[c];
+      Bs[kk][row] = rb[c];
     }
     __syncthreads();
+    if (k0 + TK < K) gload(k0 + TK);
 #pragma unroll
     for (int kk = 0; kk < TK; ++kk) {
       const float4 a = *(const float4*)&As[kk][ty * 4];
