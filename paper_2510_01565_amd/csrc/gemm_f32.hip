@@ -8,7 +8,8 @@ namespace dit {
 
 namespace {
 
-constexpr int TM = 64, TN = 64, TK = 16;
+constexpr int TM = 64, TN = 64, TK = 64;
+constexpr int LPT = TM * TK / 256;  // operand values per thread per K tile
 
 __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmProblem P) {
   __shared__ float As[TK][TM + 4];
@@ -35,16 +36,18 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmProblem P) {
   const int tx = tid & 15, ty = tid >> 4;  // 16 x 16 threads, each 4 x 4 outputs
   float acc[4][4] = {};
 
-  // 64 rows x 16 k per operand = 1024 values, 4 per thread.  The next K tile
-  // is loaded into registers while this one is multiplied; addresses are
-  // clamped into the operands (no load behind a branch, so all of them are in
-  // flight at once) and values outside them replaced by zero.
-  float ra[4], rb[4];
+  // 64 rows x 64 k per operand = 4096 values, 16 per thread (64 consecutive k
+  // of a row per wave).  The next K tile is loaded into registers while this
+  // one is multiplied; addresses are clamped into the operands (no load behind
+  // a branch, so all of them are in flight at once) and values outside them
+  // replaced by zero.
+  static_assert(TM == TN && TK == 64, "load mapping");
+  float ra[LPT], rb[LPT];
   auto gload = [&](int k0) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
+    for (int c = 0; c < LPT; ++c) {
       const int idx = tid + c * 256;
-      const int row = idx >> 4, kk = idx & 15;
+      const int row = idx >> 6, kk = idx & 63;
       const int gk = k0 + kk;
       const int am = m0 + row, bn = n0 + row;
       const float va = A[(long)min(am, M - 1) * lda + min(gk, K - 1)];
@@ -56,9 +59,9 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmProblem P) {
   gload(0);
   for (int k0 = 0; k0 < K; k0 += TK) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
+    for (int c = 0; c < LPT; ++c) {
       const int idx = tid + c * 256;
-      const int row = idx >> 4, kk = idx & 15;
+      const int row = idx >> 6, kk = idx & 63;
       As[kk][row] = ra[c];
       Bs[kk][row] = rb[c];
     }
