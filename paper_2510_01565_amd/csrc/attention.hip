@@ -261,16 +261,19 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
 }
 
 // ----------------------------------------------------------------------------
-// fp32 attention (head_dim 64) for fp32 models: one thread per query, K and V
+// fp32 attention (head_dim 64) for fp32 models: 64 queries per block, four
+// lanes per query (lane part p holds dims 16p .. 16p + 15 of q and O), K and V
 // tiles of 64 keys in LDS (rows of 16 float4, padded to 17 so the tile stores
-// of a wave spread over the banks; the compute reads are broadcasts), and the
-// online softmax taken per tile in fp32 with expf: all 64 scores of a tile
-// (independent dot products), one rescale of O and l, then O += P V.
+// of a wave spread over the banks), and the online softmax taken per tile in
+// fp32: all 64 scores of a tile (partial dot products summed over the quad),
+// one rescale of O and l, then O += P V.  exp2 of a log2(e)-scaled argument
+// adds one rounding of the argument (about 2e-6 relative at the scores met).
 constexpr int FD = 64;
 constexpr int FQ = 64;
 
-__global__ __launch_bounds__(64) void attn_f32_kernel(const AttnArgs a, const AttnSched sc) {
-  constexpr int F4 = FD / 4;
+__global__ __launch_bounds__(256) void attn_f32_kernel(const AttnArgs a, const AttnSched sc) {
+  constexpr int F4 = FD / 4;  // float4 per row
+  constexpr float kLog2e = 1.4426950408889634f;
   __shared__ float4 Ksh[64][F4 + 1];
   __shared__ float4 Vsh[64][F4 + 1];
   const int per_head = sc.tile_off[sc.n];
@@ -282,45 +285,48 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const AttnArgs a, const At
   const int q0 = (t - sc.tile_off[slot]) * FQ;
   const int L = a.meta.joint_off[r + 1] - a.meta.joint_off[r];
   const int tid = threadIdx.x;
-  const int qrow = q0 + tid;
+  const int part = tid & 3;  // the quad of a query is four consecutive lanes of one wave
+  const int qrow = q0 + (tid >> 2);
 
   const float* Qg = (const float*)a.q + (long)a.qk_off[r] * a.q_tok + (long)h * a.q_head;
   const float* Kg = (const float*)a.k + (long)a.qk_off[r] * a.k_tok + (long)h * a.k_head;
   const float* Vg = (const float*)a.vt + (long)a.vt_off[r] + (long)h * a.vt_head;
 
-  float4 q[F4], o[F4];
+  float4 q[4], o[4];
 #pragma unroll
-  for (int c = 0; c < F4; ++c) {
-    q[c] = (qrow < L) ? *(const float4*)(Qg + (long)qrow * a.q_tok + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int c = 0; c < 4; ++c) {
+    q[c] = (qrow < L) ? *(const float4*)(Qg + (long)qrow * a.q_tok + 16 * part + 4 * c)
+                      : make_float4(0.f, 0.f, 0.f, 0.f);
     o[c] = make_float4(0.f, 0.f, 0.f, 0.f);
   }
-  float m = -INFINITY, l = 0.f;
+  const float sl2 = a.scale * kLog2e;
+  float m = -INFINITY, l = 0.f;  // m in the log2 domain
   for (int kv0 = 0; kv0 < L; kv0 += 64) {
     __syncthreads();
-    // Each operand's tile arrives as 16 float4 loads per thread, all in flight
+    // Each operand's tile arrives as 4 float4 loads per thread, all in flight
     // before the LDS stores.  K rows past L re-read row L - 1 (their scores are
     // masked); V^T is read in slot order, 64 slots of the request's padded
     // columns per d, and slot s holds key vt_slot(s) (an involution).
     {
-      float4 tq[16];
+      float4 tq[4];
 #pragma unroll
-      for (int u = 0; u < 16; ++u) {
-        const int idx = tid + u * 64;
+      for (int u = 0; u < 4; ++u) {
+        const int idx = tid + u * 256;
         tq[u] = *(const float4*)(Kg + (long)min(kv0 + (idx >> 4), L - 1) * a.k_tok + (idx & 15) * 4);
       }
 #pragma unroll
-      for (int u = 0; u < 16; ++u) {
-        const int idx = tid + u * 64;
+      for (int u = 0; u < 4; ++u) {
+        const int idx = tid + u * 256;
         Ksh[idx >> 4][idx & 15] = tq[u];
       }
 #pragma unroll
-      for (int u = 0; u < 16; ++u) {
-        const int idx = tid + u * 64;
+      for (int u = 0; u < 4; ++u) {
+        const int idx = tid + u * 256;
         tq[u] = *(const float4*)(Vg + (long)(idx >> 4) * a.vt_d + kv0 + (idx & 15) * 4);
       }
 #pragma unroll
-      for (int u = 0; u < 16; ++u) {
-        const int idx = tid + u * 64, c = idx >> 4, s0 = kv0 + (idx & 15) * 4;
+      for (int u = 0; u < 4; ++u) {
+        const int idx = tid + u * 256, c = idx >> 4, s0 = kv0 + (idx & 15) * 4;
         ((float*)Vsh[vt_slot(s0) - kv0])[c] = tq[u].x;
         ((float*)Vsh[vt_slot(s0 + 1) - kv0])[c] = tq[u].y;
         ((float*)Vsh[vt_slot(s0 + 2) - kv0])[c] = tq[u].z;
@@ -333,32 +339,33 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const AttnArgs a, const At
     float mx = m;
 #pragma unroll
     for (int j = 0; j < 64; ++j) {
-      float d0 = 0.f, d1 = 0.f;
+      float d = 0.f;
 #pragma unroll
-      for (int c = 0; c < F4; c += 2) {
-        const float4 k0 = Ksh[j][c], k1 = Ksh[j][c + 1];
-        d0 = fmaf(q[c].x, k0.x, fmaf(q[c].y, k0.y, fmaf(q[c].z, k0.z, fmaf(q[c].w, k0.w, d0))));
-        d1 = fmaf(q[c + 1].x, k1.x, fmaf(q[c + 1].y, k1.y, fmaf(q[c + 1].z, k1.z, fmaf(q[c + 1].w, k1.w, d1))));
+      for (int c = 0; c < 4; ++c) {
+        const float4 k4 = Ksh[j][4 * part + c];
+        d = fmaf(q[c].x, k4.x, fmaf(q[c].y, k4.y, fmaf(q[c].z, k4.z, fmaf(q[c].w, k4.w, d))));
       }
-      s[j] = j < nk ? (d0 + d1) * a.scale : -INFINITY;
+      d += __shfl_xor(d, 1, 64);
+      d += __shfl_xor(d, 2, 64);
+      s[j] = j < nk ? d * sl2 : -INFINITY;
       mx = fmaxf(mx, s[j]);
     }
     // mx is finite: the tile holds at least one key
-    const float al = expf(m - mx);
+    const float al = exp2f(m - mx);
     float ps = 0.f;
 #pragma unroll
     for (int j = 0; j < 64; ++j) {
-      s[j] = expf(s[j] - mx);
+      s[j] = exp2f(s[j] - mx);
       ps += s[j];
     }
     l = l * al + ps;
     m = mx;
 #pragma unroll
-    for (int c = 0; c < F4; ++c) {
+    for (int c = 0; c < 4; ++c) {
       float4 acc = make_float4(o[c].x * al, o[c].y * al, o[c].z * al, o[c].w * al);
 #pragma unroll
       for (int j = 0; j < 64; ++j) {
-        const float4 v = Vsh[j][c];
+        const float4 v = Vsh[j][4 * part + c];
         acc.x = fmaf(s[j], v.x, acc.x);
         acc.y = fmaf(s[j], v.y, acc.y);
         acc.z = fmaf(s[j], v.z, acc.z);
@@ -369,10 +376,10 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const AttnArgs a, const At
   }
   if (qrow < L) {
     const int row = a.o_stream_major ? padded_to_row(a.meta, r, qrow) : a.meta.joint_off[r] + qrow;
-    float* og = (float*)a.o + (long)row * a.o_tok + (long)h * a.o_head;
+    float* og = (float*)a.o + (long)row * a.o_tok + (long)h * a.o_head + 16 * part;
     const float inv = 1.0f / l;
 #pragma unroll
-    for (int c = 0; c < F4; ++c)
+    for (int c = 0; c < 4; ++c)
       *(float4*)(og + 4 * c) = make_float4(o[c].x * inv, o[c].y * inv, o[c].z * inv, o[c].w * inv);
   }
 }
@@ -441,7 +448,7 @@ hipError_t launch_attention_f32(const AttnArgs& a, hipStream_t s) {
   const AttnSched sc = make_sched(a.meta, FQ);
   const long blocks = (long)sc.tile_off[sc.n] * a.heads;
   if (blocks == 0) return hipSuccess;
-  hipLaunchKernelGGL(attn_f32_kernel, dim3((unsigned)blocks), dim3(64), 0, s, a, sc);
+  hipLaunchKernelGGL(attn_f32_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a, sc);
   return hipGetLastError();
 }
 
