@@ -241,9 +241,9 @@ def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray,
         kh, vh = k[:, h, :], v[:, h, :]
         for r0 in range(0, qs.shape[0], q_chunk):
             s = (qs[r0:r0 + q_chunk, h, :] @ kh.T) * scale
-            s = s - s.max(axis=1, keepdims=True)
+            s -= s.max(axis=1, keepdims=True)      # in place: same values, no temporary
             p = np.exp(s)
-            p = p / p.sum(axis=1, keepdims=True)
+            p /= p.sum(axis=1, keepdims=True)
             out[r0:r0 + q_chunk, h, :] = p @ vh
     return out
 
@@ -354,18 +354,24 @@ def final_layer(params, cfg: OracleConfig, x_img: np.ndarray, c: np.ndarray, dty
 
 
 def dit_velocity(params, cfg: OracleConfig, latents: np.ndarray, text: np.ndarray,
-                 t: float, grid_hw: Tuple[int, int], dtype=F64) -> np.ndarray:
+                 t: float, grid_hw: Tuple[int, int], dtype=F64, on_block=None) -> np.ndarray:
     """One velocity prediction for one request: latents [h*w, C_in] (patchified,
-    row-major grid order), text [L_txt, D_txt] -> v [h*w, C_in]."""
+    row-major grid order), text [L_txt, D_txt] -> v [h*w, C_in].
+    ``on_block(depth, x)``, if given, sees the joint hidden state [text; image]
+    after every block (depth 0 = after the first block); it only observes."""
     c = conditioning(params, cfg, t, dtype)
     x_img = linear(np.asarray(latents, dtype), _p(params, "img_in.w", dtype), _p(params, "img_in.b", dtype))
     x_txt = linear(np.asarray(text, dtype), _p(params, "txt_in.w", dtype), _p(params, "txt_in.b", dtype))
     for i in range(cfg.n_double):
         x_txt, x_img = double_block(params, cfg, i, x_txt, x_img, c, grid_hw, dtype)
+        if on_block is not None:
+            on_block(i, np.concatenate([x_txt, x_img]))
     n_txt = x_txt.shape[0]
     x = np.concatenate([x_txt, x_img])
     for i in range(cfg.n_single):
         x = single_block(params, cfg, i, x, n_txt, c, grid_hw, dtype)
+        if on_block is not None:
+            on_block(cfg.n_double + i, x)
     return final_layer(params, cfg, x[n_txt:], c, dtype)
 
 
