@@ -116,11 +116,15 @@ typedef struct {
   int n_tensors;
 } dit_weights;
 
-/* Number of parameter tensors of a model. */
+/* Number of parameter tensors of a model (the DiT backbone of section 2.1,
+ * at the shapes of the models of section 6.1). */
 dit_status dit_weight_count(const dit_config* cfg, int* count);
 
 /*
- * Name and shape of parameter `index` (0 <= index < count).  *name points to
+ * Name and shape of parameter `index` (0 <= index < count): the parameters of
+ * the Diffusion Transformer that each denoising step runs (section 2.1, "DiT
+ * Background"; the served models of section 6.1).  The paper fixes no layout;
+ * this one is the library's own.  *name points to
  * a library-owned string valid until the library is unloaded; shape[0..ndim)
  * receives the dimensions ([out, in] for a weight, [n] for a bias).  The
  * adaLN modulation weights of all blocks are one tensor "mod.w" [rows, H] /
@@ -133,9 +137,11 @@ dit_status dit_weight_manifest(const dit_config* cfg, int index, const char** na
 
 /*
  * Bytes of device workspace that dit_step / dit_block_forward need for this
- * batch: activations, Q / K / V^T, the modulation vectors and, for bf16
- * models without DIT_FLAG_BATCH_INVARIANT, 96 MiB of split-K partial sums and
- * 4 KiB of counters (zeroed by the calls themselves; no initialisation needed).
+ * batch.  They grow with its token count: (resolution / 16)^2 image tokens per
+ * request (section 2.2, Table 1) plus its text tokens.  The workspace holds
+ * activations, Q / K / V^T, the modulation vectors and, for bf16 models
+ * without DIT_FLAG_BATCH_INVARIANT, 96 MiB of split-K partial sums and 4 KiB
+ * of counters (zeroed by the calls themselves; no initialisation needed).
  */
 dit_status dit_workspace_size(const dit_config* cfg, const dit_batch* batch, size_t* bytes);
 
@@ -153,17 +159,28 @@ dit_status dit_step(const dit_config* cfg, const dit_weights* w, const dit_batch
                     void* ws, size_t ws_bytes, void* stream);
 
 /*
- * One transformer block, in place.  kind 0 = double-stream block `index`
+ * One transformer block of the denoising network, in place (section 2.1: the
+ * step is a stack of transformer blocks whose attention spans the whole token
+ * sequence; a sequence-parallel group computes each block together).
+ * kind 0 = double-stream block `index`
  * (0 <= index < n_double), kind 1 = single-stream block `index`.
  * hidden: fp32 [sum_r n_txt + sum_r grid_h*grid_w, hidden] in stream-major
  * order, read and overwritten.  cond: fp32 device [n_req, hidden], the
  * conditioning vector c of each request (the modulation input, before SiLU).
+ * The text and image rows travel in this one fp32 buffer rather than as two
+ * separate tensors: the residual stream stays fp32 between blocks, the
+ * single-stream blocks work on the joint sequence, and a double block's text
+ * and image rows are then two contiguous row ranges of the same buffer, so no
+ * concatenation or split is needed between block kinds.
  */
 dit_status dit_block_forward(const dit_config* cfg, const dit_weights* w, int kind, int index,
                              const dit_batch* batch, float* hidden, const float* cond,
                              void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * The latent update that ends a denoising step and produces the input of the
+ * request's next step (section 4.1: a request is a chain of dependent steps;
+ * section 5, "Latent Transfer": the latents are what passes between steps).
  * Flow-matching Euler update x <- x - dt[r] * v for every request, computed in
  * fp32 and rounded once to `dtype`.  latents (in/out) and velocity:
  * [sum_r grid_h*grid_w, channels] of type dtype; dt: host array [n_req].
@@ -178,7 +195,9 @@ dit_status euler_update(const dit_batch* batch, int channels, int dtype, void* l
  * request 0's n_txt[0] text then grid_h[0]*grid_w[0] image tokens, then
  * request 1's, ...  q, k, v, o: [T_joint, heads, head_dim] of type dtype
  * (head h of token p at (p*heads + h)*head_dim).  This is the call a
- * sequence-parallel rank makes on the heads it owns after the all-to-all.
+ * sequence-parallel rank makes on the heads it owns after the all-to-all
+ * (section 2.1, Ulysses attention: tokens and heads are transposed across
+ * GPUs before local attention).
  * head_dim: 128 or 64 for DIT_BF16 (bf16 operands, fp32 softmax state and
  * accumulation, P rounded to bf16 for P V), 64 for DIT_F32 (all fp32);
  * anything else returns DIT_ERR_UNSUPPORTED before any launch.
@@ -194,7 +213,8 @@ dit_status dit_attention(const dit_batch* batch, int heads, int head_dim, int dt
  * with bf16 operands and fp32 accumulation, Y stored as fp32 (out_dtype =
  * DIT_F32) or bf16 (DIT_BF16).  b may be NULL.  dtype DIT_F32 takes fp32 X, W,
  * b and computes in fp32.  K must be a multiple of 8 and every row 16-byte
- * aligned.  Exposed so that each kernel can be checked on its own.
+ * aligned.  Exposed so that each kernel can be checked on its own; it
+ * implements no passage of the paper by itself.
  */
 dit_status dit_linear(int M, int N, int K, int dtype, const void* x, const void* w, const void* b,
                       void* y, int out_dtype, void* stream);

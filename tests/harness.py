@@ -60,3 +60,48 @@ def request_inputs(m: workloads.ModelShape, grids, n_txt, seed: int):
     lat = [synth.normal(seed, f"latents.{r}", (gh * gw, m.in_channels), bf16=bf) for r, (gh, gw) in enumerate(grids)]
     txt = [synth.normal(seed, f"text.{r}", (nt, m.text_dim), bf16=bf) for r, nt in enumerate(n_txt)]
     return lat, txt
+
+
+def upload_host_drawn_params(m: workloads.ModelShape, seed: int, workers: int = 16):
+    """Every parameter of model ``m`` drawn on the host from its seeded
+    streams (row chunks in parallel threads, as ``synth.make_params`` would
+    draw them) and copied to the device in bf16 chunk by chunk, so the host
+    never holds more than a few chunks.  Returns (dit_config, Weights)."""
+    import torch
+    from concurrent.futures import ThreadPoolExecutor
+
+    assert m.dtype == "bf16"
+    cfg = dit.make_config(m)
+    shapes = dit.weight_manifest(cfg)
+    tensors = [torch.empty(s, dtype=torch.bfloat16, device="cuda") for _, s in shapes]
+    jobs = [(ti, name, s, i) for ti, (name, s) in enumerate(shapes) for i in range(len(synth.row_chunks(s)))]
+
+    def draw(job):
+        ti, name, s, i = job
+        x = synth.normal_chunk(seed, "w:" + name, s, i, synth.WEIGHT_STD, bf16=True)
+        return ti, synth.row_chunks(s)[i], synth.bf16_bits(x)
+
+    with ThreadPoolExecutor(workers) as ex:
+        for ti, (r0, r1), bits in ex.map(draw, jobs):
+            src = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16)
+            tensors[ti][r0:r1].copy_(src)
+    torch.cuda.synchronize()
+    return cfg, dit.Weights(tensors)
+
+
+def error_histogram(got, ref) -> dict:
+    """Fractions of elements by |g - r| / max|r| (the normwise scale), and the
+    median / 99th percentile of the elementwise relative error |g - r| / |r|
+    over elements with |r| above a tenth of the rms."""
+    got = np.asarray(got, dtype=np.float64).ravel()
+    ref = np.asarray(ref, dtype=np.float64).ravel()
+    e = np.abs(got - ref) / np.abs(ref).max()
+    edges = [1e-4, 1e-3, 3e-3, 1e-2, 2e-2]
+    hist, lo = {}, 0.0
+    for hi in edges:
+        hist[f"<{hi:g}"] = float(((e >= lo) & (e < hi)).mean())
+        lo = hi
+    hist[f">={edges[-1]:g}"] = float((e >= edges[-1]).mean())
+    big = np.abs(ref) > 0.1 * np.sqrt((ref * ref).mean())
+    rel = np.abs(got - ref)[big] / np.abs(ref)[big]
+    return {"normwise_bins": hist, "rel_median": float(np.median(rel)), "rel_p99": float(np.quantile(rel, 0.99))}

@@ -1,0 +1,119 @@
+"""Whole-step parity at the workloads' full sizes: one 57-block DiT step
+(19 double + 38 single blocks, 3072 wide, 24 x 128 heads) at 1024 px, at
+2048 px and on the packed 256/512/1024/2048 px batch, against the fp64
+oracle's velocities stored in golden/fullstep/ (written by
+golden/make_fullstep_golden.py from the same seeded inputs).  The step runs
+in the benchmark's launch configuration (default flags); the velocity and
+the Euler-updated latents of every request must agree within the bf16
+tolerance, normwise.  At 1024 px the hidden state after every block, run
+block by block through dit_block_forward, is compared with the oracle's on
+sampled rows, which bounds the error's growth over the depth."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import fullstep_cases as FC
+import oracle as O
+from harness import (BF16_TOL, error_histogram, normwise_err, oracle_cfg, to_dev, upload_host_drawn_params,
+                     workspace)
+from paper_2510_01565_amd import dit, synth, workloads
+
+pytestmark = pytest.mark.gpu
+
+REPORT = os.environ.get("DIT_PARITY_REPORT")  # optional JSON lines file for the measured errors
+
+
+def _report(rec):
+    print(json.dumps(rec), flush=True)
+    if REPORT:
+        with open(REPORT, "a") as f:
+            f.write(json.dumps(rec) + "\n")
+
+
+def _golden(case, r):
+    path = FC.golden_path(case, r)
+    if not os.path.exists(path):
+        pytest.fail(f"expected values missing: {path} (run tests/golden/make_fullstep_golden.py)")
+    return np.load(path)
+
+
+@pytest.fixture(scope="module")
+def flux():
+    return upload_host_drawn_params(workloads.FLUX_FULL, FC.WEIGHT_SEED)
+
+
+@pytest.mark.parametrize("case", list(FC.CASES))
+def test_full_step_matches_oracle(flux, case):
+    import torch
+    cfg, w = flux
+    reqs = FC.requests(case)
+    ins = [FC.request_inputs(case, r) for r in range(len(reqs))]
+    b = dit.Batch([q[0] for q in reqs], [q[1] for q in reqs], [q[2] for q in reqs], [q[3] for q in reqs])
+    ws, nws = workspace(cfg, b)
+    lat = to_dev(np.concatenate([i[0] for i in ins]), torch.bfloat16)
+    txt = to_dev(np.concatenate([i[1] for i in ins]), torch.bfloat16)
+    vel = torch.full_like(lat, float("nan"))
+    print(f"full step {case}: {len(reqs)} request(s), {lat.shape[0]} image tokens", flush=True)
+    dit.dit_step(cfg, w, b, lat, txt, vel, ws, nws)
+    x_new = lat.clone()
+    dt = FC.dt(case)
+    dit.euler_update(b, cfg.in_channels, dit.DIT_BF16, x_new, vel, [dt] * len(reqs))
+    torch.cuda.synchronize()
+    got_v = vel.float().cpu().numpy()
+    got_x = x_new.float().cpu().numpy()
+    off = 0
+    for r, (gh, gw, nt, t) in enumerate(reqs):
+        g = _golden(case, r)
+        assert tuple(g["grid"]) == (gh, gw) and int(g["n_txt"]) == nt and float(g["t"]) == pytest.approx(t)
+        n = gh * gw
+        ref_v = g["velocity"].astype(np.float64)
+        ref_x = O.euler_update(ins[r][0].astype(np.float64), ref_v, dt)
+        ev = normwise_err(got_v[off:off + n], ref_v)
+        ex = normwise_err(got_x[off:off + n], ref_x)
+        _report({"case": case, "request": r, "grid": gh, "t": t, "velocity_err": ev, "latents_err": ex,
+                 "velocity_hist": error_histogram(got_v[off:off + n], ref_v)})
+        assert ev < BF16_TOL, (case, r, ev)
+        assert ex < BF16_TOL, (case, r, ex)
+        off += n
+
+
+def test_error_growth_per_block_1024px(flux):
+    """The 1024 px request block by block: embed (host, fp64), then every
+    block through dit_block_forward on the GPU's running hidden state; after
+    each block the sampled rows are compared with the oracle's."""
+    import torch
+    cfg, w = flux
+    case = FC.TRACE_CASE
+    g = _golden(case, 0)
+    rows, ref_h = g["rows"], g["hidden"]
+    m = FC.model(case)
+    (gh, gw, nt, t), = FC.requests(case)
+    lat, txt = FC.request_inputs(case, 0)
+    oc = oracle_cfg(m)
+
+    def host(name, shape):
+        return synth.normal(FC.WEIGHT_SEED, "w:" + name, shape, synth.WEIGHT_STD, bf16=True).astype(np.float64)
+
+    H = m.hidden
+    p = {n: host(n, s) for n, s in O.param_shapes(oc)
+         if n.startswith("time_in.") or n.startswith("img_in.") or n.startswith("txt_in.")}
+    c = O.conditioning(p, oc, t)
+    x_img = O.linear(lat.astype(np.float64), p["img_in.w"], p["img_in.b"])
+    x_txt = O.linear(txt.astype(np.float64), p["txt_in.w"], p["txt_in.b"])
+    b = dit.Batch([gh], [gw], [nt], [t])
+    ws, nws = workspace(cfg, b)
+    hidden = to_dev(np.concatenate([x_txt, x_img]).astype(np.float32), torch.float32)
+    cond = to_dev(c[None].astype(np.float32), torch.float32)
+    rows_d = torch.from_numpy(rows).cuda()
+    errs = []
+    for depth in range(m.n_double + m.n_single):
+        kind, idx = (0, depth) if depth < m.n_double else (1, depth - m.n_double)
+        dit.dit_block_forward(cfg, w, kind, idx, b, hidden, cond, ws, nws)
+        got = hidden[rows_d].cpu().numpy()
+        errs.append(normwise_err(got, ref_h[depth].astype(np.float64)))
+    assert ref_h.shape == (m.n_double + m.n_single, len(rows), H)
+    _report({"case": case, "per_block_err": errs,
+             "last_block_hist": error_histogram(got, ref_h[-1].astype(np.float64))})
+    assert max(errs) < BF16_TOL, errs
