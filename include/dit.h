@@ -159,6 +159,23 @@ dit_status dit_step(const dit_config* cfg, const dit_weights* w, const dit_batch
                     void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * dit_step without a workspace argument, for callers that cannot allocate
+ * device memory: code under HIP graph capture, serving loops that forbid
+ * allocation.  Same inputs, outputs, kernels and results as dit_step; the
+ * workspace is a static area of DIT_NOALLOC_SCRATCH_BYTES inside the library,
+ * one per GPU, held from the first use of the library on that GPU until the
+ * process ends.  A batch whose dit_workspace_size() exceeds that returns
+ * DIT_ERR_WORKSPACE before anything is enqueued.  The call allocates nothing
+ * (its first call on a GPU looks up that GPU's scratch address).  All calls on
+ * one GPU share its scratch and each call overwrites it: calls that overlap
+ * on one GPU (concurrent streams, or a second call enqueued on another stream
+ * before the first finishes) race and give wrong results.
+ */
+#define DIT_NOALLOC_SCRATCH_BYTES ((size_t)256 << 20)
+dit_status dit_step_noalloc(const dit_config* cfg, const dit_weights* w, const dit_batch* batch,
+                            const void* latents, const void* text_emb, void* velocity, void* stream);
+
+/*
  * One transformer block of the denoising network, in place (section 2.1: the
  * step is a stack of transformer blocks whose attention spans the whole token
  * sequence; a sequence-parallel group computes each block together).

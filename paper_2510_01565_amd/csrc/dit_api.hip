@@ -590,6 +590,120 @@ dit_status check_ws(void* ws, size_t ws_bytes, size_t need) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p) % 16 == 0; }
 
+// ---------------------------------------------------------------------------- static scratch
+// Workspace of dit_step_noalloc, for callers that cannot allocate device
+// memory (graph capture, serving loops that forbid it).  Every GPU the
+// library runs on holds its own copy until the process ends; calls on one GPU
+// share it, so calls that overlap on one GPU race.  The step clears what must
+// start at zero (split-K counters, the padding of V^T) itself.  In host code
+// `scratch` names a host-side stand-in: kernels receive the device address
+// from noalloc_scratch, never the symbol.
+constexpr size_t kNoAllocScratchBytes = DIT_NOALLOC_SCRATCH_BYTES;
+constexpr int kMaxDevices = 64;
+__device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+// Device address of `scratch` on the device that runs `stream` (the current
+// device for the null stream), looked up once per device with that device
+// current.
+dit_status noalloc_scratch(hipStream_t stream, void** out) {
+  static std::mutex mu;
+  static void* table[kMaxDevices] = {};
+  int cur = 0, dev = 0;
+  HIP_TRY(hipGetDevice(&cur));
+  dev = cur;
+  if (stream) HIP_TRY(hipStreamGetDevice(stream, &dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(DIT_ERR_UNSUPPORTED, "device %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(mu);
+  if (!table[dev]) {
+    if (dev != cur) HIP_TRY(hipSetDevice(dev));
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev != cur) HIP_TRY(hipSetDevice(cur));
+    if (e != hipSuccess) return fail(DIT_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    if (!p || ((uintptr_t)p) % 256 != 0) return fail(DIT_ERR_HIP, "static scratch address %p is not usable", p);
+    table[dev] = p;
+  }
+  *out = table[dev];
+  return DIT_OK;
+}
+// Host validation of a dit_step call; fills the batch metadata and the
+// workspace bytes the step needs.  Enqueues nothing.
+dit_status check_step(const dit_config* cfg, const dit_weights* w, const dit_batch* batch, const void* latents,
+                      const void* text_emb, const void* velocity, BatchMeta* meta, size_t* need) {
+  dit_status st;
+  if ((st = check_config(cfg)) || (st = check_batch(batch, true)) || (st = check_weights(cfg, w))) return st;
+  *meta = make_meta(batch);
+  if (!latents || !velocity || (meta->T_txt > 0 && !text_emb))
+    return fail(DIT_ERR_INVALID_ARG, "latents / text_emb / velocity is NULL");
+  if (!aligned16(latents) || !aligned16(velocity) || (text_emb && !aligned16(text_emb)))
+    return fail(DIT_ERR_INVALID_ARG, "latents / text_emb / velocity must be 16-byte aligned");
+  *need = plan_workspace(cfg, *meta, nullptr).bytes;
+  return DIT_OK;
+}
+
+// The launch sequence of one denoising step on a validated call; `ws` holds
+// at least the planned workspace.
+dit_status run_step(const dit_config* cfg, const dit_weights* w, const dit_batch* batch, const BatchMeta& meta,
+                    const void* latents, const void* text_emb, void* velocity, void* ws, void* stream) {
+  dit_status st;
+  Ctx x;
+  x.c = cfg;
+  x.L = make_layout(cfg);
+  x.meta = meta;
+  x.W = w->tensors;
+  x.ws = plan_workspace(cfg, meta, (char*)ws);
+  x.s = (hipStream_t)stream;
+  x.es = elem_size(cfg->dtype);
+  const int H = x.L.H, n = meta.n_req;
+  const int dt = cfg->dtype;
+
+  // conditioning: c = W2 SiLU(W1 e(t) + b1) + b2; all modulation vectors m = Wm SiLU(c) + bm
+  HIP_TRY(timed(x.s, "setup", 0.0, 0.0, [&] { return launch_rope_table(x.ws.rope, x.L.d, cfg->rope_theta, x.s); }));
+  HIP_TRY(timed(x.s, "setup", 0.0, 0.0,
+                [&] { return launch_zero_i32(x.ws.sk_cnt, x.ws.sk_cnt ? kSplitMaxTiles : 0, x.s); }));
+  HIP_TRY(timed(x.s, "setup", 0.0, 0.0,
+                [&] { return launch_vt_pad_zero(dt, x.ws.Vt, meta, x.L.heads, x.L.d, x.s); }));
+  HIP_TRY(timed(x.s, "setup", 0.0, 0.0,
+                [&] { return launch_timestep_embed(x.ws.temb, n, batch->t, cfg->time_freq_dim, x.s); }));
+  HIP_TRY(gemv(x.s, dt, Wt(x, 0), Wt(x, 1), x.ws.temb, cfg->time_freq_dim, n, cfg->time_freq_dim, H, 0, x.ws.u, H));
+  HIP_TRY(gemv(x.s, dt, Wt(x, 2), Wt(x, 3), x.ws.u, H, n, H, H, 1, x.ws.cvec, H));
+  HIP_TRY(gemv(x.s, dt, Wt(x, 8), Wt(x, 9), x.ws.cvec, H, n, H, x.L.mod_rows, 1, x.ws.mods, x.L.mod_rows));
+
+  // input embedders -> residual stream X (stream-major rows)
+  {
+    GemmProblem p = problem(x, H);
+    EpiArgs et = epi_base(EPI_STORE_F32, 0), ei = epi_base(EPI_STORE_F32, meta.T_txt);
+    et.out = x.ws.X;
+    ei.out = x.ws.X + (long)meta.T_txt * H;
+    et.ldo = ei.ldo = H;
+    et.bias = Wt(x, 7);
+    ei.bias = Wt(x, 5);
+    add_group(p, group(text_emb, cfg->text_dim, Wt(x, 6), cfg->text_dim, meta.T_txt, cfg->text_dim, et));
+    add_group(p, group(latents, cfg->in_channels, Wt(x, 4), cfg->in_channels, meta.T_img, cfg->in_channels, ei));
+    HIP_TRY(gemm(x, p));
+  }
+  for (int i = 0; i < cfg->n_double; ++i)
+    if ((st = run_double(x, i, x.ws.X, x.ws.mods, x.L.mod_rows, x.L.mod_dbl(i, 0), x.L.mod_dbl(i, 1)))) return st;
+  for (int i = 0; i < cfg->n_single; ++i)
+    if ((st = run_single(x, i, x.ws.X, x.ws.mods, x.L.mod_rows, x.L.mod_sgl(i)))) return st;
+
+  // final layer on the image rows -> velocity
+  const int off = x.L.mod_fin();
+  HIP_TRY(ln_mod(x, x.ws.X, meta.T_txt, meta.T, x.ws.mods, x.L.mod_rows, off, off + H, off, off + H, x.ws.A));
+  {
+    const int fb = x.L.fin();
+    GemmProblem p = problem(x, cfg->in_channels);
+    EpiArgs e = epi_base(EPI_STORE_T, meta.T_txt);
+    e.out = velocity;
+    e.ldo = cfg->in_channels;
+    e.bias = Wt(x, fb + 1);
+    add_group(p, group(x.ws.A, H, Wt(x, fb), H, meta.T_img, H, e));
+    HIP_TRY(gemm(x, p));
+  }
+  return DIT_OK;
+}
+
+
 }  // namespace
 
 // ============================================================================ C ABI
@@ -646,70 +760,27 @@ dit_status dit_step(const dit_config* cfg, const dit_weights* w, const dit_batch
                     const void* text_emb, void* velocity, void* ws, size_t ws_bytes, void* stream) {
   g_err.clear();
   dit_status st;
-  if ((st = check_config(cfg)) || (st = check_batch(batch, true)) || (st = check_weights(cfg, w))) return st;
-  const BatchMeta meta = make_meta(batch);
-  if (!latents || !velocity || (meta.T_txt > 0 && !text_emb))
-    return fail(DIT_ERR_INVALID_ARG, "latents / text_emb / velocity is NULL");
-  if (!aligned16(latents) || !aligned16(velocity) || (text_emb && !aligned16(text_emb)))
-    return fail(DIT_ERR_INVALID_ARG, "latents / text_emb / velocity must be 16-byte aligned");
-  const Workspace need = plan_workspace(cfg, meta, nullptr);
-  if ((st = check_ws(ws, ws_bytes, need.bytes))) return st;
+  BatchMeta meta;
+  size_t need = 0;
+  if ((st = check_step(cfg, w, batch, latents, text_emb, velocity, &meta, &need))) return st;
+  if ((st = check_ws(ws, ws_bytes, need))) return st;
+  return run_step(cfg, w, batch, meta, latents, text_emb, velocity, ws, stream);
+}
 
-  Ctx x;
-  x.c = cfg;
-  x.L = make_layout(cfg);
-  x.meta = meta;
-  x.W = w->tensors;
-  x.ws = plan_workspace(cfg, meta, (char*)ws);
-  x.s = (hipStream_t)stream;
-  x.es = elem_size(cfg->dtype);
-  const int H = x.L.H, n = meta.n_req;
-  const int dt = cfg->dtype;
-
-  // conditioning: c = W2 SiLU(W1 e(t) + b1) + b2; all modulation vectors m = Wm SiLU(c) + bm
-  HIP_TRY(timed(x.s, "setup", 0.0, 0.0, [&] { return launch_rope_table(x.ws.rope, x.L.d, cfg->rope_theta, x.s); }));
-  HIP_TRY(timed(x.s, "setup", 0.0, 0.0,
-                [&] { return launch_zero_i32(x.ws.sk_cnt, x.ws.sk_cnt ? kSplitMaxTiles : 0, x.s); }));
-  HIP_TRY(timed(x.s, "setup", 0.0, 0.0,
-                [&] { return launch_vt_pad_zero(dt, x.ws.Vt, meta, x.L.heads, x.L.d, x.s); }));
-  HIP_TRY(timed(x.s, "setup", 0.0, 0.0,
-                [&] { return launch_timestep_embed(x.ws.temb, n, batch->t, cfg->time_freq_dim, x.s); }));
-  HIP_TRY(gemv(x.s, dt, Wt(x, 0), Wt(x, 1), x.ws.temb, cfg->time_freq_dim, n, cfg->time_freq_dim, H, 0, x.ws.u, H));
-  HIP_TRY(gemv(x.s, dt, Wt(x, 2), Wt(x, 3), x.ws.u, H, n, H, H, 1, x.ws.cvec, H));
-  HIP_TRY(gemv(x.s, dt, Wt(x, 8), Wt(x, 9), x.ws.cvec, H, n, H, x.L.mod_rows, 1, x.ws.mods, x.L.mod_rows));
-
-  // input embedders -> residual stream X (stream-major rows)
-  {
-    GemmProblem p = problem(x, H);
-    EpiArgs et = epi_base(EPI_STORE_F32, 0), ei = epi_base(EPI_STORE_F32, meta.T_txt);
-    et.out = x.ws.X;
-    ei.out = x.ws.X + (long)meta.T_txt * H;
-    et.ldo = ei.ldo = H;
-    et.bias = Wt(x, 7);
-    ei.bias = Wt(x, 5);
-    add_group(p, group(text_emb, cfg->text_dim, Wt(x, 6), cfg->text_dim, meta.T_txt, cfg->text_dim, et));
-    add_group(p, group(latents, cfg->in_channels, Wt(x, 4), cfg->in_channels, meta.T_img, cfg->in_channels, ei));
-    HIP_TRY(gemm(x, p));
-  }
-  for (int i = 0; i < cfg->n_double; ++i)
-    if ((st = run_double(x, i, x.ws.X, x.ws.mods, x.L.mod_rows, x.L.mod_dbl(i, 0), x.L.mod_dbl(i, 1)))) return st;
-  for (int i = 0; i < cfg->n_single; ++i)
-    if ((st = run_single(x, i, x.ws.X, x.ws.mods, x.L.mod_rows, x.L.mod_sgl(i)))) return st;
-
-  // final layer on the image rows -> velocity
-  const int off = x.L.mod_fin();
-  HIP_TRY(ln_mod(x, x.ws.X, meta.T_txt, meta.T, x.ws.mods, x.L.mod_rows, off, off + H, off, off + H, x.ws.A));
-  {
-    const int fb = x.L.fin();
-    GemmProblem p = problem(x, cfg->in_channels);
-    EpiArgs e = epi_base(EPI_STORE_T, meta.T_txt);
-    e.out = velocity;
-    e.ldo = cfg->in_channels;
-    e.bias = Wt(x, fb + 1);
-    add_group(p, group(x.ws.A, H, Wt(x, fb), H, meta.T_img, H, e));
-    HIP_TRY(gemm(x, p));
-  }
-  return DIT_OK;
+dit_status dit_step_noalloc(const dit_config* cfg, const dit_weights* w, const dit_batch* batch,
+                            const void* latents, const void* text_emb, void* velocity, void* stream) {
+  g_err.clear();
+  dit_status st;
+  BatchMeta meta;
+  size_t need = 0;
+  if ((st = check_step(cfg, w, batch, latents, text_emb, velocity, &meta, &need))) return st;
+  if (need > kNoAllocScratchBytes)
+    return fail(DIT_ERR_WORKSPACE, "dit_step_noalloc: this batch needs %zu bytes of workspace, more than the "
+                "%zu bytes of the library's static scratch (use dit_step with a caller workspace)",
+                need, (size_t)kNoAllocScratchBytes);
+  void* ws = nullptr;
+  if ((st = noalloc_scratch((hipStream_t)stream, &ws))) return st;
+  return run_step(cfg, w, batch, meta, latents, text_emb, velocity, ws, stream);
 }
 
 dit_status dit_block_forward(const dit_config* cfg, const dit_weights* w, int kind, int index,

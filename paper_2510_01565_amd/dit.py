@@ -21,10 +21,11 @@ DIT_F32, DIT_BF16 = 0, 1
 DIT_MAX_REQUESTS = 16
 DIT_MAX_GRID = 256
 DIT_FLAG_BATCH_INVARIANT = 1
+DIT_NOALLOC_SCRATCH_BYTES = 256 << 20
 
-EXPORTED = ("dit_weight_count", "dit_weight_manifest", "dit_workspace_size", "dit_step", "dit_block_forward",
-            "euler_update", "dit_attention_workspace_size", "dit_attention", "dit_linear", "dit_profile_start",
-            "dit_profile_stop", "dit_profile_entry", "dit_last_error")
+EXPORTED = ("dit_weight_count", "dit_weight_manifest", "dit_workspace_size", "dit_step", "dit_step_noalloc",
+            "dit_block_forward", "euler_update", "dit_attention_workspace_size", "dit_attention", "dit_linear",
+            "dit_profile_start", "dit_profile_stop", "dit_profile_entry", "dit_last_error")
 
 
 class DitError(RuntimeError):
@@ -70,6 +71,8 @@ def lib() -> ctypes.CDLL:
                                          ctypes.POINTER(ctypes.c_size_t)]
         L.dit_step.argtypes = [ctypes.POINTER(dit_config), ctypes.POINTER(dit_weights), ctypes.POINTER(dit_batch),
                                vp, vp, vp, vp, sz, vp]
+        L.dit_step_noalloc.argtypes = [ctypes.POINTER(dit_config), ctypes.POINTER(dit_weights),
+                                       ctypes.POINTER(dit_batch), vp, vp, vp, vp]
         L.dit_block_forward.argtypes = [ctypes.POINTER(dit_config), ctypes.POINTER(dit_weights), ip, ip,
                                         ctypes.POINTER(dit_batch), vp, vp, vp, sz, vp]
         L.euler_update.argtypes = [ctypes.POINTER(dit_batch), ip, ip, vp, vp, ctypes.POINTER(ctypes.c_float), vp]
@@ -170,6 +173,11 @@ def dit_step(cfg: dit_config, w: Weights, batch: Batch, latents, text_emb, veloc
              stream=None) -> None:
     _check(lib().dit_step(ctypes.byref(cfg), ctypes.byref(w.c), ctypes.byref(batch.c), _ptr(latents),
                           _ptr(text_emb), _ptr(velocity), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def dit_step_noalloc(cfg: dit_config, w: Weights, batch: Batch, latents, text_emb, velocity, stream=None) -> None:
+    _check(lib().dit_step_noalloc(ctypes.byref(cfg), ctypes.byref(w.c), ctypes.byref(batch.c), _ptr(latents),
+                                  _ptr(text_emb), _ptr(velocity), _stream(stream)))
 
 
 def dit_block_forward(cfg: dit_config, w: Weights, kind: int, index: int, batch: Batch, hidden, cond, ws,

@@ -156,3 +156,26 @@ def test_last_error_is_cleared_by_a_good_call():
     assert dit.lib().dit_last_error().decode() != ""
     dit.weight_count(cfg)
     assert dit.lib().dit_last_error().decode() == ""
+
+
+def test_noalloc_step_rejects_batches_beyond_its_scratch_before_any_launch():
+    """dit_step_noalloc's static scratch holds DIT_NOALLOC_SCRATCH_BYTES; a
+    batch that needs more (one 1024 px request of the 57-block model) is
+    refused on the host, and so is every invalid call dit_step refuses."""
+    m = workloads.FLUX_FULL
+    cfg = dit.make_config(m)
+    n = dit.weight_count(cfg)
+    fake = dit.Weights([4096 * (i + 1) for i in range(n)])
+    P = 1 << 20
+    big = dit.Batch([64], [64], [512], [0.5])
+    assert dit.workspace_size(cfg, big) > dit.DIT_NOALLOC_SCRATCH_BYTES
+    assert _err(dit.dit_step_noalloc, cfg, fake, big, P, P, P, 0) == dit.DIT_ERR_WORKSPACE
+    assert "static scratch" in dit.lib().dit_last_error().decode()
+    small = dit.Batch([16], [16], [512], [0.5])
+    assert dit.workspace_size(cfg, small) <= dit.DIT_NOALLOC_SCRATCH_BYTES
+    assert dit.workspace_size(cfg, dit.Batch([32], [32], [512], [0.5])) <= dit.DIT_NOALLOC_SCRATCH_BYTES
+    assert _err(dit.dit_step_noalloc, cfg, fake, dit.Batch([16], [16], [512]), P, P, P, 0) == \
+        dit.DIT_ERR_INVALID_ARG
+    assert _err(dit.dit_step_noalloc, cfg, fake, small, 0, P, P, 0) == dit.DIT_ERR_INVALID_ARG
+    assert _err(dit.dit_step_noalloc, cfg, dit.Weights([4096] * (n - 1)), small, P, P, P, 0) == \
+        dit.DIT_ERR_INVALID_ARG
