@@ -54,12 +54,48 @@ int64_t step_time_of(const int64_t* step_us, int32_t gpus) {
   return j < TS_MAX_DEGREES ? step_us[j] : 0;
 }
 
-struct Opt {
-  int32_t m;       // kNone or allocation index
-  int32_t width;   // w_i(o)
-  int32_t steps;   // q_i^m
-  int32_t sv;      // survives to the next round start
+// One thing a request can do in the coming round (section 4.2.2): stay idle
+// (alloc = kNone, no GPUs), or run one of its planned allocations for as many
+// of that allocation's steps as fit in the round.  `alive`: whether it can
+// still meet its deadline afterwards, if every step it has left then ran at
+// its fastest degree.
+struct Choice {
+  int32_t alloc;
+  int32_t gpus;
+  int32_t steps;
+  int32_t alive;
 };
+
+// What a packing achieves: requests kept alive first, then fewer GPUs (GPUs
+// left over go to late requests and to scale-up).
+struct Value {
+  int32_t alive = 0;
+  int32_t gpus = 0;
+};
+bool better(const Value& a, const Value& b) { return a.alive != b.alive ? a.alive > b.alive : a.gpus < b.gpus; }
+bool same(const Value& a, const Value& b) { return a.alive == b.alive && a.gpus == b.gpus; }
+
+std::vector<Choice> round_choices(const ts_request& r, int32_t n_gpus, int64_t round_us, int64_t round_end_us) {
+  int64_t fastest = 0;
+  for (int j : usable_degrees(r.step_us, TS_MAX_DEGREES, n_gpus))
+    if (fastest == 0 || r.step_us[j] < fastest) fastest = r.step_us[j];
+  // steps of each allocation that fit in one round
+  std::vector<int32_t> fit(r.n_allocs, 0);
+  for (int m = 0; m < r.n_allocs; ++m) {
+    const int64_t t = step_time_of(r.step_us, r.allocs[m].gpus);
+    if (t > 0) fit[m] = int32_t(std::min<int64_t>(r.allocs[m].steps, round_us / t));
+  }
+  // alive after running `ran` steps of allocation `m` (none for kNone)
+  auto alive_after = [&](int32_t m) {
+    int64_t left = 0;
+    for (int a = 0; a < r.n_allocs; ++a) left += r.allocs[a].steps - (a == m ? fit[a] : 0);
+    return int32_t(round_end_us + left * fastest <= r.deadline_us);
+  };
+  std::vector<Choice> out{Choice{kNone, 0, 0, alive_after(kNone)}};
+  for (int m = 0; m < r.n_allocs; ++m)
+    if (fit[m] > 0 && r.allocs[m].gpus <= n_gpus) out.push_back(Choice{m, r.allocs[m].gpus, fit[m], alive_after(m)});
+  return out;
+}
 
 }  // namespace
 
@@ -144,86 +180,64 @@ extern "C" ts_status ts_round_schedule(const ts_request* reqs, int32_t n_req, in
       if (r.allocs[m].steps < 0 || r.allocs[m].gpus < 1) return TS_ERR_INVALID_ARG;
     if (usable_degrees(r.step_us, TS_MAX_DEGREES, n_gpus).empty()) return TS_ERR_INVALID_ARG;
   }
-  const int64_t t_next = now_us + round_us;
-
-  // option sets O_i with width, progress and survival (the loop before the DP)
-  std::vector<std::vector<Opt>> opts(n_req);
-  std::vector<int64_t> left(n_req);
+  const int64_t round_end = now_us + round_us;
+  std::vector<std::vector<Choice>> choices(n_req);
+  std::vector<int64_t> steps_left(n_req, 0);
   for (int i = 0; i < n_req; ++i) {
-    const ts_request& r = reqs[i];
-    int64_t t_min = 0;
-    for (int j : usable_degrees(r.step_us, TS_MAX_DEGREES, n_gpus))
-      if (t_min == 0 || r.step_us[j] < t_min) t_min = r.step_us[j];
-    std::vector<int32_t> q(r.n_allocs);
-    int64_t total = 0;
-    for (int m = 0; m < r.n_allocs; ++m) {
-      const int64_t t = step_time_of(r.step_us, r.allocs[m].gpus);
-      q[m] = t > 0 ? int32_t(std::min<int64_t>(r.allocs[m].steps, round_us / t)) : 0;
-      total += r.allocs[m].steps;
-    }
-    left[i] = total;
-    auto survival = [&](int32_t m) {
-      int64_t rem = 0;
-      for (int mm = 0; mm < r.n_allocs; ++mm) rem += std::max<int64_t>(0, r.allocs[mm].steps - (mm == m ? q[mm] : 0));
-      return int32_t(t_next + rem * t_min <= r.deadline_us);
-    };
-    opts[i].push_back(Opt{kNone, 0, 0, survival(kNone)});
-    for (int m = 0; m < r.n_allocs; ++m)
-      if (q[m] > 0 && r.allocs[m].gpus <= n_gpus) opts[i].push_back(Opt{m, r.allocs[m].gpus, q[m], survival(m)});
+    choices[i] = round_choices(reqs[i], n_gpus, round_us, round_end);
+    for (int m = 0; m < reqs[i].n_allocs; ++m) steps_left[i] += reqs[i].allocs[m].steps;
   }
 
-  // group knapsack over capacity: dp[c] = most survivors with exactly c GPUs
-  // in use (-1: unreachable); choice[i][c] = option of request i on that path
+  // Pack one choice per request into the N GPUs, maximising the requests kept
+  // alive (a knapsack with one group of choices per request).  best[i][g] is
+  // the best Value of requests i.. on at most g GPUs, filled from the last
+  // request backwards.
   const int N = n_gpus;
-  std::vector<int32_t> dp(N + 1, -1), nxt(N + 1);
-  dp[0] = 0;
-  std::vector<std::vector<uint8_t>> choice(n_req, std::vector<uint8_t>(N + 1, 0));
-  for (int i = 0; i < n_req; ++i) {
-    nxt = dp;
-    for (int c = 0; c <= N; ++c)
-      for (size_t o = 0; o < opts[i].size(); ++o) {
-        const Opt& op = opts[i][o];
-        if (op.width > c || dp[c - op.width] < 0) continue;
-        const int32_t cand = dp[c - op.width] + op.sv;
-        if (cand > nxt[c]) {
-          nxt[c] = cand;
-          choice[i][c] = uint8_t(o);
-        }
+  std::vector<std::vector<Value>> best(n_req + 1, std::vector<Value>(N + 1));
+  for (int i = n_req - 1; i >= 0; --i)
+    for (int g = 0; g <= N; ++g) {
+      bool set = false;
+      for (const Choice& ch : choices[i]) {
+        if (ch.gpus > g) continue;
+        const Value& rest = best[i + 1][g - ch.gpus];
+        const Value v{ch.alive + rest.alive, ch.gpus + rest.gpus};
+        if (!set || better(v, best[i][g])) best[i][g] = v;
+        set = true;
       }
-    dp.swap(nxt);
-  }
-  int c_star = 0;
-  for (int c = 1; c <= N; ++c)
-    if (dp[c] > dp[c_star]) c_star = c;
-
-  // plan from the back-pointers
+    }
+  // Read the plan forwards: each request takes its first choice (idle, then
+  // allocations in order) that still reaches the best value.
   int32_t used = 0;
-  for (int i = n_req - 1, c = c_star; i >= 0; --i) {
-    const Opt& op = opts[i][choice[i][c]];
-    out[i] = ts_decision{op.m, op.width, op.steps, op.sv, 0};
-    c -= op.width;
-    used += op.width;
+  for (int i = 0, g = N; i < n_req; ++i) {
+    for (const Choice& ch : choices[i]) {
+      if (ch.gpus > g) continue;
+      const Value& rest = best[i + 1][g - ch.gpus];
+      if (same(Value{ch.alive + rest.alive, ch.gpus + rest.gpus}, best[i][g])) {
+        out[i] = ts_decision{ch.alloc, ch.gpus, ch.steps, ch.alive, 0};
+        g -= ch.gpus;
+        used += ch.gpus;
+        break;
+      }
+    }
   }
 
-  // best effort: requests none of whose options survives, earliest deadline
-  // first, one leftover GPU each
+  // Requests that cannot stay alive whatever they run get one leftover GPU
+  // each, earliest deadline first, for the steps that fit in the round.
   std::vector<int> late;
-  for (int i = 0; i < n_req; ++i) {
-    bool any = false;
-    for (const Opt& op : opts[i]) any = any || op.sv;
-    if (!any) late.push_back(i);
-  }
+  for (int i = 0; i < n_req; ++i)
+    if (std::none_of(choices[i].begin(), choices[i].end(), [](const Choice& ch) { return ch.alive != 0; }))
+      late.push_back(i);
   std::stable_sort(late.begin(), late.end(),
                    [&](int a, int b) { return reqs[a].deadline_us < reqs[b].deadline_us; });
   for (int i : late) {
     if (used >= N) break;
     const int64_t t1 = reqs[i].step_us[0];
-    const int64_t q1 = t1 > 0 ? std::min<int64_t>(left[i], round_us / t1) : 0;
+    const int64_t q1 = t1 > 0 ? std::min<int64_t>(steps_left[i], round_us / t1) : 0;
     if (q1 <= 0 || out[i].gpus != 0) continue;
     out[i] = ts_decision{kNone, 1, int32_t(q1), 0, 1};
     used += 1;
   }
-  *survivors = n_req > 0 ? dp[c_star] : 0;
+  *survivors = n_req > 0 ? best[0][N].alive : 0;
   *gpus_used = used;
   return TS_OK;
 }
