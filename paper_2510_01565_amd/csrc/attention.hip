@@ -54,12 +54,13 @@ __device__ __forceinline__ void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt((7 <<
 
 // NW waves x 32 queries per block, head dimension HD (64 or 128).
 //
-// Pipeline over 64-key tiles j: K and V^T tiles arrive by direct-to-LDS loads
-// (global_load_lds_dwordx4) in a ring of STAGES buffers, issued STAGES - 1
-// tiles ahead; each tile runs scores, softmax, P V in turn.
+// Pipeline over 64-key tiles j: K and V^T tiles arrive by direct-to-LDS buffer
+// loads in two stages, tile j + 1 loading while tile j runs scores, softmax
+// and P V in turn.
 template <int NW, int HD, int STAGES>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
+  static_assert(STAGES == 2, "two LDS stages, the loop is unrolled over them");
   constexpr int BQ = NW * 32;
   static_assert(HD == 64 || HD == 128, "head dim");
   constexpr int CH = HD / 8;       // 16-byte chunks per key row of the K tile
@@ -90,35 +91,55 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
   const bf16_t* __restrict__ Qg = (const bf16_t*)a.q + (long)a.qk_off[r] * a.q_tok + (long)h * a.q_head;
   const bf16_t* __restrict__ Kg = (const bf16_t*)a.k + (long)a.qk_off[r] * a.k_tok + (long)h * a.k_head;
   const bf16_t* __restrict__ Vg = (const bf16_t*)a.vt + (long)a.vt_off[r] + (long)h * a.vt_head;
+  const int Lpad = a.vt_off[r + 1] - a.vt_off[r];
 
-  // K rows past L are clamped to the last key (their scores are masked); V^T
-  // columns past L are in the request's padding, which holds zeros.
-  auto tile_load = [&](int j, int st) {
+  // K and V^T tiles move by range-checked buffer loads straight into LDS
+  // (64 lanes x 16 bytes per wave instruction, no registers).  Each lane's
+  // byte offset inside a tile is fixed here; a tile only moves the buffer's
+  // base.  Keys past L fall outside the K buffer of the tile and read as
+  // zeros (their scores are masked); V^T columns past L lie in the request's
+  // zeroed padding.
+  int kvo[KI], vvo[VI];
+#pragma unroll
+  for (int q = 0; q < KI; ++q) {
+    const int key = (wave * KI + q) * KPI + lane / CH;
+    kvo[q] = (key * (int)a.k_tok + kswz(key, lane % CH) * 8) * 2;
+  }
+#pragma unroll
+  for (int q = 0; q < VI; ++q) {
+    const int dr = (wave * VI + q) * 8 + (lane >> 3);
+    vvo[q] = (dr * (int)a.vt_d + ((lane & 7) ^ ((dr >> 1) & 7)) * 8) * 2;
+  }
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  char* const lbase = (char*)&smem[0][0];
+  constexpr int STAGE_B = (KT_U4 + VT_U4) * 16;
+  auto tile_load = [&](int j, auto stc) __attribute__((always_inline)) {
+    constexpr int st = decltype(stc)::value;
     const int kv0 = j * BKV;
-    uint4* S = smem[st];
+    const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(Kg + (long)kv0 * a.k_tok), (short)0, ((L - 1 - kv0) * (int)a.k_tok + HD) * 2, kBufferWord3);
+    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(Vg + kv0), (short)0, ((HD - 1) * (int)a.vt_d + Lpad - kv0) * 2, kBufferWord3);
 #pragma unroll
     for (int q = 0; q < KI; ++q) {
-      const int k0 = (wave * KI + q) * KPI;
-      const int key = k0 + lane / CH, sl = lane % CH;
-      const bf16_t* g = Kg + (long)min(kv0 + key, L - 1) * a.k_tok + kswz(key, sl) * 8;
-      __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)(S + k0 * CH), 16, 0,
-                                       0);
+      const int vo = kvo[q];
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rk, (__attribute__((address_space(3))) void*)(lbase + st * STAGE_B + (wv * KI + q) * KPI * CH * 16), 16,
+          vo, 0, 0, 0);
     }
 #pragma unroll
     for (int q = 0; q < VI; ++q) {
-      const int d0 = (wave * VI + q) * 8;
-      const int dr = d0 + (lane >> 3), sl = lane & 7;
-      const bf16_t* g = Vg + (long)dr * a.vt_d + kv0 + (sl ^ ((dr >> 1) & 7)) * 8;
-      __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)(S + KT_U4 + d0 * 8),
-                                       16, 0, 0);
+      const int vo = vvo[q];
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rv, (__attribute__((address_space(3))) void*)(lbase + st * STAGE_B + KT_U4 * 16 + (wv * VI + q) * 8 * 8 * 16),
+          16, vo, 0, 0, 0);
     }
   };
 
   const int ntiles = (L + BKV - 1) / BKV;
-  // prologue: the first STAGES - 1 tiles in flight
-#pragma unroll
-  for (int t = 0; t < STAGES - 1; ++t)
-    if (t < ntiles) tile_load(t, t);
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  tile_load(0, S0{});
 
   // Q fragments (B operand of S^T = K Q^T): query q0 + wave*32 + lane%32, d chunk 2*ks + lane/32
   const int qrow = q0 + wave * 32 + (lane & 31);
@@ -140,8 +161,27 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
 
   // S^T of one 64-key tile: two 32x32 blocks (keys kb*32 + (i/4)*8 + hl*4 + i%4 of
   // register i, query lane % 32)
-  auto scores = [&](int st, f32x16_t* s) {
-    const uint4* S = smem[st];
+  // Per-lane LDS byte offsets of the fragment reads, fixed before the loop:
+  // K fragment of k-step ks (key lane % 32 of key block 0; key block 1 is
+  // 32 rows further) and V^T fragment of key step ks2 (d row lane % 32 of d
+  // block 0; d block db is 32 rows further).  Stage and block offsets are
+  // immediates of the reads.
+  int kfo[HD / 16], vfo[4];
+#pragma unroll
+  for (int ks = 0; ks < HD / 16; ++ks) kfo[ks] = ((lane & 31) * CH + kswz(lane & 31, ks * 2 + hl)) * 16;
+#pragma unroll
+  for (int ks2 = 0; ks2 < 4; ++ks2) {
+    const int dr = lane & 31;
+    vfo[ks2] = KT_U4 * 16 + (dr * 8 + ((ks2 * 2 + hl) ^ ((dr >> 1) & 7))) * 16;
+  }
+  auto lds_frag = [&](int byte_off) __attribute__((always_inline)) {
+    return __builtin_bit_cast(bf16x8_t, *(const uint4*)(lbase + byte_off));
+  };
+
+  // S^T of one 64-key tile: two 32x32 blocks (keys kb*32 + (i/4)*8 + hl*4 + i%4 of
+  // register i, query lane % 32)
+  auto scores = [&](auto stc, f32x16_t* s) __attribute__((always_inline)) {
+    constexpr int st = decltype(stc)::value;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -150,9 +190,9 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
     for (int ks = 0; ks < HD / 16; ++ks) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        const int key = kb * 32 + (lane & 31);
-        const uint4 u = S[key * CH + kswz(key, ks * 2 + hl)];
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, u), qf[ks], s[kb], 0, 0, 0);
+        // key kb*32 + lane%32 keeps the swizzle term of key lane%32 (kb*32 is a multiple of 16)
+        const bf16x8_t u = lds_frag(kfo[ks] + st * STAGE_B + kb * 32 * CH * 16);
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(u, qf[ks], s[kb], 0, 0, 0);
       }
     }
     // keep four fragment reads ahead of the MFMAs that consume them
@@ -189,7 +229,8 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
   // exceeds 2^RESCALE_SLACK (or overflows, as on the first tile) is the true
   // row max formed, the max raised, O and l rescaled, and the tile redone.
   // O and l always share the max they were computed with, so O / l is exact.
-  auto softmax_pv = [&](int j, int st, f32x16_t* s) {
+  auto softmax_pv = [&](int j, auto stc, f32x16_t* s) __attribute__((always_inline)) {
+    constexpr int st = decltype(stc)::value;
     const int kv0 = j * BKV;
     if (kv0 + BKV > L) {
 #pragma unroll
@@ -220,27 +261,40 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
       t = exps_pack(s, pf);
     }
     l_i += t;
-    const uint4* V = smem[st] + KT_U4;
 #pragma unroll
     for (int ks2 = 0; ks2 < 4; ++ks2) {
 #pragma unroll
       for (int db = 0; db < HD / 32; ++db) {
-        const int dr = db * 32 + (lane & 31);
-        const uint4 u = V[dr * 8 + ((ks2 * 2 + hl) ^ ((dr >> 1) & 7))];
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, u), pf[ks2], o[db], 0, 0, 0);
+        // d row db*32 + lane%32 keeps the swizzle term of row lane%32
+        const bf16x8_t u = lds_frag(vfo[ks2] + st * STAGE_B + db * 32 * 8 * 16);
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(u, pf[ks2], o[db], 0, 0, 0);
       }
     }
     sched_read_ahead<4 * HD / 32, 4>();
   };
+  // Tile j sits in stage j % 2.  Each tile starts with the loads of tile
+  // j + 1 into the other stage (freed by the barrier that ended tile j - 1)
+  // and ends with this wave's loads landed and a bare barrier: after it every
+  // wave's part of tile j + 1 is in LDS and no wave reads tile j any more.
+  // (A __syncthreads() fence would drain nothing more but costs a wait on
+  // every outstanding memory operation.)
   f32x16_t sc_t[2];
-  for (int j = 0; j < ntiles; ++j) {
-    // tile j resident for every wave; every wave is done with tile j - 1
+  wait_vmcnt0();
+  asm volatile("s_barrier" ::: "memory");
+  auto step = [&](int j, auto stc) __attribute__((always_inline)) {
+    constexpr int st = decltype(stc)::value;
+    if (j + 1 < ntiles) tile_load(j + 1, std::integral_constant<int, st ^ 1>{});
+    scores(stc, sc_t);
+    softmax_pv(j, stc, sc_t);
     wait_vmcnt0();
-    __syncthreads();
-    if (j + STAGES - 1 < ntiles) tile_load(j + STAGES - 1, (j + STAGES - 1) % STAGES);
-    scores(j % STAGES, sc_t);
-    softmax_pv(j, j % STAGES, sc_t);
+    asm volatile("s_barrier" ::: "memory");
+  };
+  int j = 0;
+  for (; j + 1 < ntiles; j += 2) {
+    step(j, S0{});
+    step(j + 1, S1{});
   }
+  if (j < ntiles) step(j, S0{});
 
   const float l = l_i + __shfl_xor(l_i, 32, 64);
   if (qrow < L) {

@@ -238,6 +238,11 @@ __device__ __forceinline__ void epilogue_segment16(const EpiArgs& e, const RowEn
 
 // XCD-aware block remap: hardware dispatches block b to XCD b % 8; return an
 // index such that every XCD owns one contiguous range of indices.
+// Word 3 of a raw buffer resource on gfx9-family targets: 32-bit data format,
+// so untyped dword loads are range-checked against num_records and return
+// zeros past it.
+constexpr int kBufferWord3 = 0x00020000;
+
 __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
   const int per = nblocks / 8, rem = nblocks % 8;
   const int xcd = bid % 8, idx = bid / 8;

@@ -65,10 +65,6 @@ __device__ __forceinline__ int lds_slot(int row, int kc) {
 
 // s_waitcnt with vmcnt = n and the other counters left alone (gfx9 encoding:
 // vmcnt[3:0] and [15:14], expcnt[6:4], lgkmcnt[11:8]).
-// Word 3 of a raw buffer resource on gfx9-family targets: 32-bit data format,
-// so untyped dword loads are range-checked against num_records and return
-// zeros past it.
-constexpr int kBufferWord3 = 0x00020000;
 
 template <int n>
 __device__ __forceinline__ void wait_vmcnt() {

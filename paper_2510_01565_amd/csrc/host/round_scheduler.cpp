@@ -1,5 +1,5 @@
 // Round-based step scheduler of TetriServe (section 4.2): deadline-aware GPU
-// allocation of one request and the per-round request packing of Algorithm 1.
+// allocation of one request and the per-round packing of requests onto GPUs.
 // Host code only; the C ABI is declared in include/tetri_sched.h.
 #include "../../../include/tetri_sched.h"
 
