@@ -136,7 +136,7 @@ __device__ __forceinline__ void epilogue_element(const EpiArgs& e, const RowEntr
       else if (which == 1)
         ((T*)e.k)[((long)h * e.T + row.pos) * d + dd] = from_f32<T>(v);
       else
-        ((T*)e.vt)[((long)h * d + dd) * e.T + vt_slot(row.pos)] = from_f32<T>(v);
+        ((T*)e.vt)[((long)h * d + dd) * e.vt_ld + vt_slot(row.pos)] = from_f32<T>(v);
       break;
     }
     default:
@@ -225,9 +225,9 @@ __device__ __forceinline__ void epilogue_segment16(const EpiArgs& e, const RowEn
       else if (which == 1)
         store16<T>((T*)e.k + ((long)h * e.T + row.pos) * d + dd0, v);
       else {
-        T* vt = (T*)e.vt + ((long)h * d + dd0) * e.T + vt_slot(row.pos);
+        T* vt = (T*)e.vt + ((long)h * d + dd0) * e.vt_ld + vt_slot(row.pos);
 #pragma unroll
-        for (int q = 0; q < 16; ++q) vt[(long)q * e.T] = from_f32<T>(v[q]);
+        for (int q = 0; q < 16; ++q) vt[(long)q * e.vt_ld] = from_f32<T>(v[q]);
       }
       break;
     }

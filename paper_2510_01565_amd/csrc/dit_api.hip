@@ -254,15 +254,22 @@ struct Workspace {
   float* cvec;   // [n_req, H]
   float2* rope;  // [DIT_MAX_GRID, d/4]
   float* X;      // [T, H] residual stream
-  void* A;       // [T, H] LayerNorm output
+  void* A;       // [T, H] LayerNorm output, row pitch lda
   void* Q;       // [heads, Tp, d]
   void* K;       // [heads, Tp, d]
-  void* Vt;      // [heads, d, Tp]
-  void* Z;       // [T, H + F]  attention output | MLP hidden
+  void* Vt;      // [heads, d, Tp], row pitch ldvt
+  void* Z;       // [T, H + F]  attention output | MLP hidden, row pitch ldz
+  long lda, ldz, ldvt;  // row pitches in elements (see kRowPad)
   float* sk_part;  // partial sums of split GEMMs (kSplitPartBytes), null when GEMMs never split
   int* sk_cnt;     // their arrival counters [kSplitMaxTiles], zeroed at the start of every call
   size_t bytes;
 };
+
+// Row pitches of the activations that GEMMs and attention stream (A, Z, V^T)
+// are padded by 64 elements past their width.  With unpadded pitches (6 KB,
+// 30 KB, 9 KB, 33 KB ...: multiples of 4 KB or of 2 KB) the rows of one
+// operand tile fall on few L2 channels; the padding spreads them.
+constexpr long kRowPad = 64;
 
 Workspace plan_workspace(const dit_config* c, const BatchMeta& m, char* base) {
   const Layout L = make_layout(c);
@@ -281,11 +288,14 @@ Workspace plan_workspace(const dit_config* c, const BatchMeta& m, char* base) {
   w.cvec = (float*)take(n * L.H * 4);
   w.rope = (float2*)take((size_t)DIT_MAX_GRID * (L.d / 4) * sizeof(float2));
   w.X = (float*)take(T * L.H * 4);
-  w.A = take(T * L.H * es);
+  w.lda = L.H + kRowPad;
+  w.ldz = L.H + L.F + kRowPad;
+  w.ldvt = (long)Tp + kRowPad;
+  w.A = take(T * w.lda * es);
   w.Q = take((size_t)L.heads * Tp * L.d * es);
   w.K = take((size_t)L.heads * Tp * L.d * es);
-  w.Vt = take((size_t)L.heads * Tp * L.d * es);
-  w.Z = take(T * (size_t)(L.H + L.F) * es);
+  w.Vt = take((size_t)L.heads * L.d * w.ldvt * es);
+  w.Z = take(T * (size_t)w.ldz * es);
   const bool split = c->dtype == DIT_BF16 && !(c->flags & DIT_FLAG_BATCH_INVARIANT);
   w.sk_part = split ? (float*)take(kSplitPartBytes) : nullptr;
   w.sk_cnt = split ? (int*)take(kSplitMaxTiles * sizeof(int)) : nullptr;
@@ -382,7 +392,7 @@ hipError_t ln_mod(const Ctx& x, const float* X, int row_begin, int row_end, cons
   const double bytes = (double)(row_end - row_begin) * H * (4 + x.es);
   return timed(x.s, "ln_modulate", 0.0, bytes, [&] {
     return launch_ln_modulate(x.c->dtype, X, H, row_begin, row_end, x.meta, mods, mods_ld, sh_t, sc_t, sh_i, sc_i,
-                              x.c->ln_eps, out, H, x.s);
+                              x.c->ln_eps, out, x.ws.lda, x.s);
   });
 }
 
@@ -437,12 +447,13 @@ EpiArgs epi_qkv(const Ctx& x, int row_base) {
   e.k = x.ws.K;
   e.vt = x.ws.Vt;
   e.T = x.meta.pad_off[x.meta.n_req];
+  e.vt_ld = x.ws.ldvt;
   e.hidden = x.L.H;
   e.head_dim = x.L.d;
   e.n_qkv = 3 * x.L.H;
   e.rope = x.ws.rope;
-  e.gelu_out = (char*)x.ws.Z + (long)row_base * (x.L.H + x.L.F) * x.es;
-  e.gelu_ld = x.L.H + x.L.F;
+  e.gelu_out = (char*)x.ws.Z + (long)row_base * x.ws.ldz * x.es;
+  e.gelu_ld = x.ws.ldz;
   e.gelu_col0 = x.L.H;
   return e;
 }
@@ -468,10 +479,10 @@ hipError_t attention(const Ctx& x) {
   a.k_tok = x.L.d;
   a.k_head = Tp * x.L.d;
   a.vt = x.ws.Vt;
-  a.vt_head = (long)x.L.d * Tp;
-  a.vt_d = Tp;
+  a.vt_head = (long)x.L.d * x.ws.ldvt;
+  a.vt_d = x.ws.ldvt;
   a.o = x.ws.Z;
-  a.o_tok = x.L.H + x.L.F;
+  a.o_tok = x.ws.ldz;
   a.o_head = x.L.d;
   a.o_stream_major = 1;
   a.heads = x.L.heads;
@@ -490,7 +501,7 @@ dit_status run_double(const Ctx& x, int i, float* X, const float* mods, int mods
   const int H = x.L.H, F = x.L.F, Tt = x.meta.T_txt, Ti = x.meta.T_img, T = x.meta.T, es = x.es;
   const int bi = x.L.dbl(i, 0), bt = x.L.dbl(i, 1);
   const float eps = x.c->ln_eps;
-  const long ldz = H + F;
+  const long ldz = x.ws.ldz, lda = x.ws.lda;
   // 1. adaLN (shift1, scale1)
   HIP_TRY(ln_mod(x, X, 0, T, mods, mods_ld, off_txt, off_txt + H, off_img, off_img + H, x.ws.A));
   // 2. QKV projections (+ RoPE on image rows), scattered into the joint Q/K/V^T layout
@@ -499,8 +510,8 @@ dit_status run_double(const Ctx& x, int i, float* X, const float* mods, int mods
     EpiArgs et = epi_qkv(x, 0), ei = epi_qkv(x, Tt);
     et.bias = Wt(x, bt + 1);
     ei.bias = Wt(x, bi + 1);
-    add_group(p, group(x.ws.A, H, Wt(x, bt), H, Tt, H, et));
-    add_group(p, group(elem_ptr(x.ws.A, (long)Tt * H, es), H, Wt(x, bi), H, Ti, H, ei));
+    add_group(p, group(x.ws.A, lda, Wt(x, bt), H, Tt, H, et));
+    add_group(p, group(elem_ptr(x.ws.A, (long)Tt * lda, es), lda, Wt(x, bi), H, Ti, H, ei));
     HIP_TRY(gemm(x, p));
   }
   // 3. joint attention -> Z[:, 0:H]
@@ -529,8 +540,8 @@ dit_status run_double(const Ctx& x, int i, float* X, const float* mods, int mods
     et.col0 = ei.col0 = H;
     et.bias = Wt(x, bt + 5);
     ei.bias = Wt(x, bi + 5);
-    add_group(p, group(x.ws.A, H, Wt(x, bt + 4), H, Tt, H, et));
-    add_group(p, group(elem_ptr(x.ws.A, (long)Tt * H, es), H, Wt(x, bi + 4), H, Ti, H, ei));
+    add_group(p, group(x.ws.A, lda, Wt(x, bt + 4), H, Tt, H, et));
+    add_group(p, group(elem_ptr(x.ws.A, (long)Tt * lda, es), lda, Wt(x, bi + 4), H, Ti, H, ei));
     HIP_TRY(gemm(x, p));
   }
   // 7. MLP down + gated residual (gate2)
@@ -550,13 +561,13 @@ dit_status run_double(const Ctx& x, int i, float* X, const float* mods, int mods
 dit_status run_single(const Ctx& x, int i, float* X, const float* mods, int mods_ld, int off) {
   const int H = x.L.H, F = x.L.F, T = x.meta.T;
   const int b = x.L.sgl(i);
-  const long ldz = H + F;
+  const long ldz = x.ws.ldz;
   HIP_TRY(ln_mod(x, X, 0, T, mods, mods_ld, off, off + H, off, off + H, x.ws.A));
   {
     GemmProblem p = problem(x, 3 * H + F);
     EpiArgs e = epi_qkv(x, 0);
     e.bias = Wt(x, b + 1);
-    add_group(p, group(x.ws.A, H, Wt(x, b), H, T, H, e));
+    add_group(p, group(x.ws.A, x.ws.lda, Wt(x, b), H, T, H, e));
     HIP_TRY(gemm(x, p));
   }
   HIP_TRY(attention(x));
@@ -662,7 +673,7 @@ dit_status run_step(const dit_config* cfg, const dit_weights* w, const dit_batch
   HIP_TRY(timed(x.s, "setup", 0.0, 0.0,
                 [&] { return launch_zero_i32(x.ws.sk_cnt, x.ws.sk_cnt ? kSplitMaxTiles : 0, x.s); }));
   HIP_TRY(timed(x.s, "setup", 0.0, 0.0,
-                [&] { return launch_vt_pad_zero(dt, x.ws.Vt, meta, x.L.heads, x.L.d, x.s); }));
+                [&] { return launch_vt_pad_zero(dt, x.ws.Vt, x.ws.ldvt, meta, x.L.heads, x.L.d, x.s); }));
   HIP_TRY(timed(x.s, "setup", 0.0, 0.0,
                 [&] { return launch_timestep_embed(x.ws.temb, n, batch->t, cfg->time_freq_dim, x.s); }));
   HIP_TRY(gemv(x.s, dt, Wt(x, 0), Wt(x, 1), x.ws.temb, cfg->time_freq_dim, n, cfg->time_freq_dim, H, 0, x.ws.u, H));
@@ -697,7 +708,7 @@ dit_status run_step(const dit_config* cfg, const dit_weights* w, const dit_batch
     e.out = velocity;
     e.ldo = cfg->in_channels;
     e.bias = Wt(x, fb + 1);
-    add_group(p, group(x.ws.A, H, Wt(x, fb), H, meta.T_img, H, e));
+    add_group(p, group(x.ws.A, x.ws.lda, Wt(x, fb), H, meta.T_img, H, e));
     HIP_TRY(gemm(x, p));
   }
   return DIT_OK;
@@ -811,7 +822,7 @@ dit_status dit_block_forward(const dit_config* cfg, const dit_weights* w, int ki
   HIP_TRY(timed(x.s, "setup", 0.0, 0.0,
                 [&] { return launch_zero_i32(x.ws.sk_cnt, x.ws.sk_cnt ? kSplitMaxTiles : 0, x.s); }));
   HIP_TRY(timed(x.s, "setup", 0.0, 0.0,
-                [&] { return launch_vt_pad_zero(cfg->dtype, x.ws.Vt, meta, x.L.heads, x.L.d, x.s); }));
+                [&] { return launch_vt_pad_zero(cfg->dtype, x.ws.Vt, x.ws.ldvt, meta, x.L.heads, x.L.d, x.s); }));
   if (kind == 0) {
     // this block's modulation rows: image stream, then (untied) text stream
     const int off = x.L.mod_dbl(index, 0);
@@ -876,7 +887,7 @@ dit_status dit_attention(const dit_batch* batch, int heads, int head_dim, int dt
   hipStream_t s = (hipStream_t)stream;
   HIP_TRY(timed(s, "v_transpose", 0.0, 2.0 * m.T * heads * head_dim * elem_size(dtype),
                 [&] { return launch_v_transpose(dtype, v, m, heads, head_dim, ws, s); }));
-  HIP_TRY(timed(s, "v_transpose", 0.0, 0.0, [&] { return launch_vt_pad_zero(dtype, ws, m, heads, head_dim, s); }));
+  HIP_TRY(timed(s, "v_transpose", 0.0, 0.0, [&] { return launch_vt_pad_zero(dtype, ws, m.pad_off[m.n_req], m, heads, head_dim, s); }));
   AttnArgs a;
   memset(&a, 0, sizeof(a));
   const long Tp = m.pad_off[m.n_req];

@@ -106,7 +106,8 @@ struct EpiArgs {
   void* q;              // [heads][T][d]
   void* k;              // [heads][T][d]
   void* vt;             // [heads][d][T], column vt_slot(padded position)
-  int T;                // padded joint length (pad_off[n_req])
+  int T;                // padded joint length (pad_off[n_req]): Q / K rows per head
+  long vt_ld;           // row pitch of V^T in elements (>= T)
   int hidden;
   int head_dim;
   int n_qkv;            // 3 * hidden
@@ -197,6 +198,6 @@ hipError_t launch_v_transpose(int dtype, const void* v, const BatchMeta& meta, i
 // n ints at p set to zero (a fill kernel, so a captured graph holds no memset node)
 hipError_t launch_zero_i32(int* p, int n, hipStream_t s);
 // zeroes the V^T columns of the padding keys of every request (padded positions >= the request length)
-hipError_t launch_vt_pad_zero(int dtype, void* vt, const BatchMeta& meta, int heads, int d, hipStream_t s);
+hipError_t launch_vt_pad_zero(int dtype, void* vt, long ld, const BatchMeta& meta, int heads, int d, hipStream_t s);
 
 }  // namespace dit

@@ -276,8 +276,7 @@ hipError_t launch_zero_i32(int* p, int n, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_vt_pad_zero(int dtype, void* vt, const BatchMeta& meta, int heads, int d, hipStream_t s) {
-  const long ld = meta.pad_off[meta.n_req];
+hipError_t launch_vt_pad_zero(int dtype, void* vt, long ld, const BatchMeta& meta, int heads, int d, hipStream_t s) {
   const dim3 grid((unsigned)(heads * d));
   if (dtype == DIT_BF16)
     hipLaunchKernelGGL(vt_pad_zero_kernel<bf16_t>, grid, dim3(64), 0, s, (bf16_t*)vt, meta, ld);

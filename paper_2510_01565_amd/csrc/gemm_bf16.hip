@@ -530,7 +530,7 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
           const RowEntry r0 = rows[ml0];
           const bool whole = m + 15 < M && (r0.pos & 15) == 0 && rows[ml0 + 15].pos == r0.pos + 15;
           const int hn = n - 2 * E.hidden, h = hn / E.head_dim, dd = hn - h * E.head_dim;
-          bf16_t* vt = (bf16_t*)E.vt + ((long)h * E.head_dim + dd) * E.T;
+          bf16_t* vt = (bf16_t*)E.vt + ((long)h * E.head_dim + dd) * E.vt_ld;
           if (whole) {
             // slot s of the group holds key vt_slot(s): swap the middle quads
             float w[16];
