@@ -51,6 +51,9 @@ __device__ __forceinline__ void sched_read_ahead() {
 
 // s_waitcnt with vmcnt = 0 and the other counters left alone (gfx9 encoding).
 __device__ __forceinline__ void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); }
+// s_waitcnt with vmcnt = 0 and lgkmcnt = 0: this wave's tile loads have
+// landed and its LDS fragment reads have returned
+__device__ __forceinline__ void wait_vmcnt0_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(7 << 4); }
 
 // NW waves x 32 queries per block, head dimension HD (64 or 128).
 //
@@ -281,12 +284,16 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
   f32x16_t sc_t[2];
   wait_vmcnt0();
   asm volatile("s_barrier" ::: "memory");
+  // The wait before the barrier also covers the LDS reads: the compiler may
+  // place the last P V MFMAs (and the waits for their V^T fragments) after the
+  // barrier, and the stage those fragments come from is reloaded right after
+  // it by the other waves.
   auto step = [&](int j, auto stc) __attribute__((always_inline)) {
     constexpr int st = decltype(stc)::value;
     if (j + 1 < ntiles) tile_load(j + 1, std::integral_constant<int, st ^ 1>{});
     scores(stc, sc_t);
     softmax_pv(j, stc, sc_t);
-    wait_vmcnt0();
+    wait_vmcnt0_lgkmcnt0();
     asm volatile("s_barrier" ::: "memory");
   };
   int j = 0;

@@ -364,10 +364,11 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
       // of the tile to arrive -- add every piece's in piece order (the same
       // order whichever piece arrives last) and go on to the epilogue.  A
       // piece that finds all the others already counted skips publishing.
-      // Only thread 0 orders memory: the block barrier completes every wave's
-      // stores first, and only a block that reads the others' sums acquires
-      // (an acquire invalidates the L2 of its XCD, which blocks still
-      // multiplying there depend on).
+      // Only thread 0 orders memory: every wave waits for its own stores
+      // before the block barrier, thread 0 then releases at agent scope
+      // (writing the XCD's L2 back) and counts, and only a block that reads
+      // the others' sums acquires (an acquire invalidates the L2 of its XCD,
+      // which blocks still multiplying there depend on).
       constexpr int NV = AM * AN;
       int* const flag = (int*)&lds[STAGES * STAGE - 1];  // past the epilogue's LDS (asserted below)
       int* const cnt = P.sk_cnt + tile_id;
@@ -387,9 +388,17 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
             const f32x4_t a4 = acc16[i][j];
             mine[(i * AN + j) * NT + tid] = make_float4(a4[0], a4[1], a4[2], a4[3]);
           }
+        // every wave's partial sums reach L2 before the barrier: the block
+        // barrier alone does not wait for other waves' stores, and thread 0's
+        // release below only waits for its own wave's
+        wait_vmcnt<0>();
         __syncthreads();
         if (tid == 0) {
-          const bool last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT) == np - 1;
+          // release: the XCD's L2 written back, and the write-back complete,
+          // before the count
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+          wait_vmcnt<0>();
+          const bool last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == np - 1;
           if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
           *flag = last;
         }
