@@ -329,6 +329,18 @@ def roofline(kernels, dtype: str, workload: str):
             **common}
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
 def cpu_baseline(wl, seed: int):
     """The oracle (fp64, as it stands) on a bounded sample of the workload:
     one double-stream and one single-stream block at the workload's token
@@ -363,6 +375,7 @@ def cpu_baseline(wl, seed: int):
     t_s = time.perf_counter() - t0
     t_step = m.n_double * t_d + m.n_single * t_s
     return {"value": 1.0 / t_step, "unit": "steps/s", "cores": threads or os.cpu_count(), "kind": "oracle",
+            "nproc": os.cpu_count(), "cpu_model": cpu_model(),
             "sample": f"oracle (numpy fp64) on one double-stream ({t_d:.2f} s) and one single-stream block "
                       f"({t_s:.2f} s) at {nt} text + {gh * gh} image tokens, extrapolated to "
                       f"{m.n_double} + {m.n_single} blocks ({t_step:.1f} s per step)",
@@ -381,7 +394,9 @@ def main() -> int:
                     help="comma-separated further workloads reported under per_workload (default: the other "
                          "resolutions of the paper's mix, one GPU's share of the 4-way 2048 px split, the packed "
                          "mixed-resolution batch, one double block and the small fp32 block; '' for none)")
-    ap.add_argument("--extra-steps", type=int, default=3)
+    ap.add_argument("--extra-steps", type=int, default=10,
+                    help="timed steps of each further workload (after --extra-warmup untimed ones)")
+    ap.add_argument("--extra-warmup", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy-gib", type=float, default=0.0,
@@ -418,6 +433,7 @@ def main() -> int:
     log(f"{wl.name}: {main_res['ms_per_step']:.2f} ms/step, {main_res['tflops']:.1f} TFLOP/s "
         f"({100 * main_res['frac_peak']:.1f}% of peak), CV {main_res['cv_pct']:.2f}%")
     per = {wl.name: {k: v for k, v in main_res.items() if k != "kernels"}}
+    per[wl.name]["steps"], per[wl.name]["warmup"] = args.steps, args.warmup
     models = {wl.model: (cfg, w)}
     for name in [x for x in args.extra.split(",") if x]:
         ow = workloads.WORKLOADS[name]
@@ -438,12 +454,20 @@ def main() -> int:
             continue
         if ow.kind != "step":
             continue
-        r = run_workload(torch, dit, synth, workloads, ow, cfg, w, args.extra_steps, 1, args.seed, dev,
-                         profile=False)
-        log(f"{name}: {r['ms_per_step']:.2f} ms/step, {r['tflops']:.1f} TFLOP/s ({100 * r['frac_peak']:.1f}% of peak)")
+        r = run_workload(torch, dit, synth, workloads, ow, cfg, w, args.extra_steps, args.extra_warmup, args.seed,
+                         dev, profile=True)
+        r["steps"], r["warmup"] = args.extra_steps, args.extra_warmup
+        r["roofline"] = roofline(r["kernels"], ow.model.dtype, ow.name)
+        r["roofline"]["step_frac_of_peak"] = r["frac_peak"]
+        log(f"{name}: {r['ms_per_step']:.2f} ms/step, {r['tflops']:.1f} TFLOP/s ({100 * r['frac_peak']:.1f}% of peak), "
+            f"CV {r['cv_pct']:.2f}%; dominant kernel {r['roofline']['kernel']} at "
+            f"{100 * r['roofline']['frac']:.1f}% of its roofline")
         per[name] = {k: v for k, v in r.items() if k != "kernels"}
 
     rl = roofline(main_res["kernels"], wl.model.dtype, wl.name)
+    # the whole step's share of the peak beside the dominant kernel's
+    rl["step_frac_of_peak"] = main_res["frac_peak"]
+    per[wl.name]["roofline"] = rl
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
