@@ -152,11 +152,14 @@ def measured_traffic(family: str, workload: str):
 
 
 def run_sp_share(torch, dit, synth, workloads, wl, cfg, w, steps, seed, dev):
-    """One GPU's share of a k-way (Ulysses) sequence-parallel step at real shape,
-    composed from measured launches: every non-attention kernel of a step on
-    the rank's token shard (L/k tokens: n_txt/k text + grid^2/k image), plus
-    one attention per block over all L tokens for n_heads/k heads -- the
-    all-to-alls between them are not part of a one-GPU measurement."""
+    """One GPU's share of a k-way (Ulysses) sequence-parallel step at real shape:
+    every non-attention kernel of a step on the rank's token shard (L/k tokens:
+    n_txt/k text + grid^2/k image), plus one attention per block over all L
+    tokens for n_heads/k heads -- the all-to-alls between them are not part of
+    a one-GPU measurement.  Both parts are HIP-event-timed loops: the shard's
+    whole step (dit_step + euler_update) minus the attention it runs on its own
+    tokens (taken from one profiled step), and the block count of dit_attention
+    calls on the rank's heads (each with the V transpose a rank would need)."""
     k = wl.extra.get("sp", 4)
     m = wl.model
     g = wl.grids()[0]
@@ -169,18 +172,31 @@ def run_sp_share(torch, dit, synth, workloads, wl, cfg, w, steps, seed, dev):
     txt = synth.device_normal(seed, "text:share", (n_txt_shard, m.text_dim), 1.0, torch.bfloat16, dev)
     vel = torch.empty_like(lat)
     stream = torch.cuda.current_stream()
-    for _ in range(2):
-        dit.dit_step(cfg, w, b, lat, txt, vel, ws, nws, stream)
-    torch.cuda.synchronize()
-    dit.profile_start()
-    for _ in range(steps):
+
+    def shard_step():
         dit.dit_step(cfg, w, b, lat, txt, vel, ws, nws, stream)
         dit.euler_update(b, m.in_channels, dit.DIT_BF16, lat, vel, [wl.dt], stream)
+
+    def timed_loop(fn, n):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(n):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    for _ in range(3):
+        shard_step()
+    shard_ms = timed_loop(shard_step, steps)
+    dit.profile_start()
+    shard_step()
     torch.cuda.synchronize()
     kern = dit.profile_stop()
-    non_attn_ms = sum(v["ms"] for n, v in kern.items()
-                      if not n.startswith("attention") and not n.startswith("detail:")) / steps
-    # attention of the rank's heads over the whole sequence
+    shard_attn_ms = sum(v["ms"] for n, v in kern.items() if n.startswith("attention"))
+    non_attn_ms = shard_ms - shard_attn_ms
+    # attention of the rank's heads over the whole sequence, once per block
     heads = m.heads // k
     L = wl.n_txt[0] + g * g
     ab = dit.Batch([g], [g], [wl.n_txt[0]])
@@ -190,24 +206,25 @@ def run_sp_share(torch, dit, synth, workloads, wl, cfg, w, steps, seed, dev):
     o = torch.empty_like(q)
     anws = dit.attention_workspace_size(ab, heads, m.head_dim, dit.DIT_BF16)
     aws = torch.empty(anws, dtype=torch.uint8, device=dev)
-    dit.dit_attention(ab, heads, m.head_dim, dit.DIT_BF16, q, kk, v, o, aws, anws, stream)
-    torch.cuda.synchronize()
     nblk = m.n_double + m.n_single
-    dit.profile_start()
-    for _ in range(nblk):
-        dit.dit_attention(ab, heads, m.head_dim, dit.DIT_BF16, q, kk, v, o, aws, anws, stream)
-    torch.cuda.synchronize()
-    akern = dit.profile_stop()
-    attn_ms = sum(x["ms"] for n, x in akern.items() if n.startswith("attention"))
+
+    def attn_blocks():
+        for _ in range(nblk):
+            dit.dit_attention(ab, heads, m.head_dim, dit.DIT_BF16, q, kk, v, o, aws, anws, stream)
+
+    attn_blocks()
+    attn_ms = timed_loop(attn_blocks, max(1, steps // 2))
     share_ms = non_attn_ms + attn_ms
     fl = workloads.flops_per_step(m, [n_txt_shard], [shard_grid[0] * shard_grid[1]])
     attn_flops = nblk * 4.0 * L * L * m.head_dim * heads
     total = fl["gemm"] + attn_flops
     return {"steps_per_s": 1e3 / share_ms, "ms_per_step": share_ms, "non_attention_ms": non_attn_ms,
-            "attention_ms": attn_ms, "tflop_per_step": total / 1e12, "tflops": total / (share_ms / 1e3) / 1e12,
+            "attention_ms": attn_ms, "shard_step_ms": shard_ms, "shard_step_attention_ms": shard_attn_ms,
+            "tflop_per_step": total / 1e12, "tflops": total / (share_ms / 1e3) / 1e12,
             "frac_peak": total / (share_ms / 1e3) / 1e12 / BF16_PEAK_TFLOPS,
-            "note": f"composed: non-attention kernels of a step on the {L // k}-token shard + {nblk} attention "
-                    f"launches of {heads} heads over {L} tokens (HIP events); all-to-alls excluded"}
+            "note": f"composed from HIP-event-timed loops: the {L // k}-token shard's step minus its own attention "
+                    f"(profiled), plus {nblk} dit_attention calls of {heads} heads over {L} tokens (V transpose "
+                    f"included); all-to-alls excluded"}
 
 
 def block_flops(m, n_txt, n_img) -> dict:
