@@ -482,20 +482,29 @@ hipError_t launch_attn_cfg(const AttnArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Measured on MI355X: a software pipeline that issues tile j + 1's score MFMAs
-// before tile j's softmax needs 255 VGPRs and loses to the plain order at 2
-// waves per SIMD, so the plain order with 2 buffers is used.
+// Measured on MI355X: software pipelines that overlap a tile's softmax with
+// the next tile's score MFMAs (255 VGPRs, spills) or with the previous tile's
+// P V MFMAs (separate K and V^T rings of 2 or 4 stages, ~205 VGPRs) gave the
+// same bits and were no faster where attention matters most (16 896 tokens),
+// so the plain order with 2 buffers is used.
 template <int HD>
 hipError_t launch_attn_hd(const AttnArgs& a, hipStream_t s) {
-  // 128 queries per block, two blocks per CU: the two waves of a SIMD belong
-  // to different blocks and drift apart (one in its softmax while the other
-  // issues MFMAs), measured on MI355X +10% at 16 896 tokens and +1.5% at
-  // 4 608 tokens over one block of 256 queries per CU.  At head dim 64 (half
-  // the registers, so two 256-query blocks fit on a CU) the 256-query blocks
-  // stay ahead until the launch has many blocks.
+  // Blocks of 128 queries (4 waves), two per CU: the two waves of a SIMD
+  // belong to different blocks and drift apart (one in its softmax while the
+  // other issues MFMAs); blocks of 256 queries (8 waves), one per CU at head
+  // dim 128, read each K/V tile once for twice the queries.  Measured on
+  // MI355X over whole 57-block steps (in-process A/B, head dim 128): 256-query
+  // blocks win when the launch has 256 to 2047 units of 128 queries x heads
+  // (512 px: 288 units, -0.9% per step; 1024 px: 864 units, -1.1%) and lose
+  // with fewer (256 px: 144 units, too few blocks to fill the CUs, +1.8%) or
+  // more (2048 px: 3168 units, +1.3%; the packed 256-2048 px batch: 4464,
+  // +0.6%).  At head dim 64 (half the registers, so two 256-query blocks fit
+  // on a CU) the 256-query blocks stay ahead until the launch has 2048 units.
   const AttnSched sc4 = make_sched(a.meta, 4 * 32);
-  if (HD == 128 || (long)sc4.tile_off[sc4.n] * a.heads >= 2048) return launch_attn_cfg<4, HD>(a, s);
-  return launch_attn_cfg<8, HD>(a, s);
+  const long units = (long)sc4.tile_off[sc4.n] * a.heads;
+  const bool wide = HD == 128 ? (units >= 256 && units < 2048) : units < 2048;
+  if (wide) return launch_attn_cfg<8, HD>(a, s);
+  return launch_attn_cfg<4, HD>(a, s);
 }
 
 hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s) {
