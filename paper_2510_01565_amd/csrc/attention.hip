@@ -487,22 +487,38 @@ hipError_t launch_attn_cfg(const AttnArgs& a, hipStream_t s) {
 // P V MFMAs (separate K and V^T rings of 2 or 4 stages, ~205 VGPRs) gave the
 // same bits and were no faster where attention matters most (16 896 tokens),
 // so the plain order with 2 buffers is used.
+// Block shape at head dim 128.  Blocks of 128 queries (4 waves) run two per
+// CU; their last round of a launch holds the leftover blocks, and when these
+// are at most one per CU each runs alone on its CU, much faster than as one
+// of two.  Blocks of 256 queries (8 waves, one per CU) read each K/V tile once
+// for twice the queries but get no such lone tail.  So with U units (128
+// queries x heads) on 2 x 256 block slots, the 128-query blocks win when the
+// last round is at most half full (frac(U / 512) <= 1/2) and the 256-query
+// blocks otherwise.  Measured on MI355X (in-process A/B) at 16 896 tokens:
+// 6 heads (U = 792) 256-query blocks -11%, 12 heads (1584) +4%, 18 heads
+// (2376) -7%, 24 heads (3168) +2%; at 4608 tokens: 24 heads (864) -4%,
+// 48 heads (1728) +3%; whole steps at 256 px (144) +1.8% and 512 px (288)
+// -0.9%.  The rule assumes equal units, i.e. requests of one length; for a
+// batch of mixed lengths (longest first, so the last round holds the short
+// units) the 128-query blocks are kept (the packed 256-2048 px step: +0.6%
+// with 256-query blocks).  At head dim 64 (half the registers, so two
+// 256-query blocks fit on a CU) the 256-query blocks stay ahead until the
+// launch has 2048 units.
 template <int HD>
 hipError_t launch_attn_hd(const AttnArgs& a, hipStream_t s) {
-  // Blocks of 128 queries (4 waves), two per CU: the two waves of a SIMD
-  // belong to different blocks and drift apart (one in its softmax while the
-  // other issues MFMAs); blocks of 256 queries (8 waves), one per CU at head
-  // dim 128, read each K/V tile once for twice the queries.  Measured on
-  // MI355X over whole 57-block steps (in-process A/B, head dim 128): 256-query
-  // blocks win when the launch has 256 to 2047 units of 128 queries x heads
-  // (512 px: 288 units, -0.9% per step; 1024 px: 864 units, -1.1%) and lose
-  // with fewer (256 px: 144 units, too few blocks to fill the CUs, +1.8%) or
-  // more (2048 px: 3168 units, +1.3%; the packed 256-2048 px batch: 4464,
-  // +0.6%).  At head dim 64 (half the registers, so two 256-query blocks fit
-  // on a CU) the 256-query blocks stay ahead until the launch has 2048 units.
   const AttnSched sc4 = make_sched(a.meta, 4 * 32);
   const long units = (long)sc4.tile_off[sc4.n] * a.heads;
-  const bool wide = HD == 128 ? (units >= 256 && units < 2048) : units < 2048;
+  bool wide;
+  if (HD == 128) {
+    bool equal = true;
+    const int L0 = a.meta.joint_off[sc4.req[0] + 1] - a.meta.joint_off[sc4.req[0]];
+    for (int i = 1; i < sc4.n; ++i)
+      equal = equal && a.meta.joint_off[sc4.req[i] + 1] - a.meta.joint_off[sc4.req[i]] == L0;
+    constexpr long kSlots = 2 * 256;  // 128-query blocks resident per GPU (two per CU, 256 CUs)
+    wide = equal && 2 * (units % kSlots) > kSlots;
+  } else {
+    wide = units < 2048;
+  }
   if (wide) return launch_attn_cfg<8, HD>(a, s);
   return launch_attn_cfg<4, HD>(a, s);
 }
