@@ -558,6 +558,23 @@ dit_status run_double(const Ctx& x, int i, float* X, const float* mods, int mods
   return DIT_OK;
 }
 
+// Rows of an M x N GEMM (N a multiple of 256) that fill whole rounds of
+// 256 x 256 tiles on the 256 CUs, when the rest would leave a last round at
+// most a quarter full (0: no such split).  At 2048 px the single blocks'
+// linear2 (16 896 x 3072) is 16 384 rows in 3 rounds and a 24-tile remainder.
+int full_round_rows(int M, int N) {
+  constexpr int kCUs = 256, kTile = 256;
+  if (N % kTile != 0) return 0;
+  const int tn = N / kTile;
+  int unit = 1;  // row tiles per whole number of rounds: 256 / gcd(tn, 256)
+  while ((unit * tn) % kCUs != 0) ++unit;
+  const long rows_unit = (long)unit * kTile;
+  const long M1 = (M / rows_unit) * rows_unit;
+  const long rest_tiles = (long)((M - M1 + kTile - 1) / kTile) * tn;
+  if (M1 == 0 || M1 == M || 4 * rest_tiles > kCUs) return 0;
+  return (int)M1;
+}
+
 dit_status run_single(const Ctx& x, int i, float* X, const float* mods, int mods_ld, int off) {
   const int H = x.L.H, F = x.L.F, T = x.meta.T;
   const int b = x.L.sgl(i);
@@ -572,10 +589,19 @@ dit_status run_single(const Ctx& x, int i, float* X, const float* mods, int mods
   }
   HIP_TRY(attention(x));
   {
+    // Rows [0, T1) form whole rounds of 256 x 256 tiles; a short remainder
+    // [T1, T) becomes a second group, which the launch model may run as a
+    // launch of its own with K split across the otherwise idle CUs.
     GemmProblem p = problem(x, H);
+    const int T1 = full_round_rows(T, H);
     EpiArgs e = epi_resid(x, X, 0, mods, mods_ld, off + 2 * H);
     e.bias = Wt(x, b + 3);
-    add_group(p, group(x.ws.Z, ldz, Wt(x, b + 2), H + F, T, H + F, e));
+    add_group(p, group(x.ws.Z, ldz, Wt(x, b + 2), H + F, T1 > 0 ? T1 : T, H + F, e));
+    if (T1 > 0) {
+      EpiArgs e2 = epi_resid(x, X, T1, mods, mods_ld, off + 2 * H);
+      e2.bias = Wt(x, b + 3);
+      add_group(p, group(elem_ptr(x.ws.Z, (long)T1 * ldz, x.es), ldz, Wt(x, b + 2), H + F, T - T1, H + F, e2));
+    }
     HIP_TRY(gemm(x, p));
   }
   return DIT_OK;
