@@ -89,9 +89,12 @@ typedef struct {
  * DIT_FLAG_BATCH_INVARIANT: every output bit of a request is independent of
  * what it is packed with.  Without it, a bf16 GEMM launch with too few output
  * tiles to fill the GPU may split its K range over several blocks whose fp32
- * partial sums are added in a fixed order; results stay bitwise identical from
- * run to run, but the order of the sums (and so the last bits) can change with
- * the batch composition.  The flag also removes the split's workspace.
+ * partial sums are added in a fixed order, and a bf16 attention launch whose
+ * last round of 128-query tiles is at most a quarter full may split those tiles'
+ * key ranges (head dim 128, requests of one length); results stay bitwise
+ * identical from run to run, but the order of the sums (and so the last bits)
+ * can change with the batch composition.  The flag also removes the split's
+ * workspace.
  */
 #define DIT_FLAG_BATCH_INVARIANT 1
 
@@ -218,7 +221,11 @@ dit_status euler_update(const dit_batch* batch, int channels, int dtype, void* l
  * head_dim: 128 or 64 for DIT_BF16 (bf16 operands, fp32 softmax state and
  * accumulation, P rounded to bf16 for P V), 64 for DIT_F32 (all fp32);
  * anything else returns DIT_ERR_UNSUPPORTED before any launch.
- * ws: at least dit_attention_workspace_size() bytes.
+ * ws: at least dit_attention_workspace_size() bytes: V^T, plus for DIT_BF16
+ * at head_dim 128, when the last round of 128-query tiles (two per CU) is at
+ * most a quarter full after two or more full rounds and every request has one
+ * length, the fp32 partial results of those tiles' key ranges (up to 33 MiB),
+ * merged in a fixed order (bitwise repeatable).
  */
 dit_status dit_attention_workspace_size(const dit_batch* batch, int heads, int head_dim, int dtype,
                                         size_t* bytes);

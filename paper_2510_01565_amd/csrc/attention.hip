@@ -16,6 +16,8 @@
 // K/V tiles are shared through that XCD's L2.
 #include <math.h>
 
+#include <algorithm>
+
 #include "device_common.h"
 
 namespace dit {
@@ -29,7 +31,6 @@ struct AttnSched {
   int tile_off[kMaxReq + 1]; // prefix sum of q-tiles per head
 };
 
-constexpr int BKV = 64;  // keys per tile
 // Lazy rescaling: the running max used for exp2 is only raised when a new
 // score exceeds it by more than 2^RESCALE_SLACK; until then probabilities may
 // reach 2^8, which fp32 and bf16 hold exactly as well as any other value.
@@ -55,31 +56,47 @@ __device__ __forceinline__ void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt((7 <<
 // landed and its LDS fragment reads have returned
 __device__ __forceinline__ void wait_vmcnt0_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(7 << 4); }
 
-// NW waves x 32 queries per block, head dimension HD (64 or 128).
+// NW waves x 32 queries per block, head dimension HD (64 or 128), BKV keys
+// (64 or 128) per tile.
 //
-// Pipeline over 64-key tiles j: K and V^T tiles arrive by direct-to-LDS buffer
+// Pipeline over key tiles j: K and V^T tiles arrive by direct-to-LDS buffer
 // loads in two stages, tile j + 1 loading while tile j runs scores, softmax
 // and P V in turn.
-template <int NW, int HD, int STAGES>
+template <int NW, int HD, int STAGES, int BKV>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
   static_assert(STAGES == 2, "two LDS stages, the loop is unrolled over them");
   constexpr int BQ = NW * 32;
   static_assert(HD == 64 || HD == 128, "head dim");
+  static_assert(BKV == 64 || BKV == 128, "key tile");
   constexpr int CH = HD / 8;       // 16-byte chunks per key row of the K tile
   constexpr int KPI = 64 / CH;     // keys per load instruction (64 lanes x 16 bytes)
-  constexpr int KT_U4 = BKV * CH;  // K tile: [64 keys][CH chunks of 8 d], chunk slot swizzled by kswz
-  constexpr int VT_U4 = HD * 8;    // V^T tile: [HD d][8 chunks of 8 key slots], chunk slot ^= (d >> 1) & 7
+  constexpr int VCH = BKV / 8;     // 16-byte chunks per d row of the V^T tile
+  constexpr int VRPI = 64 / VCH;   // V^T rows per load instruction
+  constexpr int KT_U4 = BKV * CH;  // K tile: [BKV keys][CH chunks of 8 d], chunk slot swizzled by kswz
+  constexpr int VT_U4 = HD * VCH;  // V^T tile: [HD d][VCH chunks of 8 key slots], chunk slot swizzled by vswz
   constexpr int KI = BKV / KPI / NW;  // K-tile load instructions per wave
-  constexpr int VI = HD / 8 / NW;     // V^T-tile load instructions per wave (8 rows each)
-  static_assert(KI * KPI * NW == BKV && VI * 8 * NW == HD, "tile config");
-  // slot of chunk c in key row `key`: the 16 keys one ds_read_b128 serves per
-  // cycle land on 16 different 16-byte bank groups (an involution in c)
+  constexpr int VI = HD / VRPI / NW;  // V^T-tile load instructions per wave
+  static_assert(KI * KPI * NW == BKV && VI * VRPI * NW == HD, "tile config");
+  // slot of chunk c in key row `key` / V^T row `dr`: the 16 rows one
+  // ds_read_b128 serves per cycle land on 16 different 16-byte bank groups
+  // (an involution in c)
   auto kswz = [](int key, int c) { return HD == 128 ? c ^ (key & 15) : c ^ ((key >> 1) & 7); };
+  auto vswz = [](int dr, int c) { return BKV == 128 ? c ^ (dr & 15) : c ^ ((dr >> 1) & 7); };
   __shared__ uint4 smem[STAGES][KT_U4 + VT_U4];
 
   const int per_head = sc.tile_off[sc.n];
-  const int id = xcd_remap(blockIdx.x, gridDim.x);
+  // unit (query tile x head) of this block and, on a key-split launch, its
+  // key range: blocks of one XCD take consecutive indices, and a split
+  // launch numbers the pieces key range first, so the blocks of one XCD
+  // share K/V ranges
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  int piece = 0, id = bid;
+  if (a.kv_pieces > 1) {
+    piece = bid / a.units;
+    id = bid - piece * a.units;
+  }
+  id += a.unit0;
   const int h = id / per_head;
   const int t = id - h * per_head;
   int slot = 0;
@@ -110,8 +127,8 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
   }
 #pragma unroll
   for (int q = 0; q < VI; ++q) {
-    const int dr = (wave * VI + q) * 8 + (lane >> 3);
-    vvo[q] = (dr * (int)a.vt_d + ((lane & 7) ^ ((dr >> 1) & 7)) * 8) * 2;
+    const int dr = (wave * VI + q) * VRPI + lane / VCH;
+    vvo[q] = (dr * (int)a.vt_d + vswz(dr, lane % VCH) * 8) * 2;
   }
   const int wv = __builtin_amdgcn_readfirstlane(wave);
   char* const lbase = (char*)&smem[0][0];
@@ -134,15 +151,18 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
     for (int q = 0; q < VI; ++q) {
       const int vo = vvo[q];
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rv, (__attribute__((address_space(3))) void*)(lbase + st * STAGE_B + KT_U4 * 16 + (wv * VI + q) * 8 * 8 * 16),
+          rv, (__attribute__((address_space(3))) void*)(lbase + st * STAGE_B + KT_U4 * 16 + (wv * VI + q) * VRPI * VCH * 16),
           16, vo, 0, 0, 0);
     }
   };
 
-  const int ntiles = (L + BKV - 1) / BKV;
+  // key tiles [jb, je) of this block (all of them unless the keys are split)
+  const int nt_all = (L + BKV - 1) / BKV;
+  const int jb = piece * nt_all / a.kv_pieces;
+  const int je = (piece + 1) * nt_all / a.kv_pieces;
   using S0 = std::integral_constant<int, 0>;
   using S1 = std::integral_constant<int, 1>;
-  tile_load(0, S0{});
+  tile_load(jb, S0{});
 
   // Q fragments (B operand of S^T = K Q^T): query q0 + wave*32 + lane%32, d chunk 2*ks + lane/32
   const int qrow = q0 + wave * 32 + (lane & 31);
@@ -169,37 +189,37 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
   // 32 rows further) and V^T fragment of key step ks2 (d row lane % 32 of d
   // block 0; d block db is 32 rows further).  Stage and block offsets are
   // immediates of the reads.
-  int kfo[HD / 16], vfo[4];
+  int kfo[HD / 16], vfo[BKV / 16];
 #pragma unroll
   for (int ks = 0; ks < HD / 16; ++ks) kfo[ks] = ((lane & 31) * CH + kswz(lane & 31, ks * 2 + hl)) * 16;
 #pragma unroll
-  for (int ks2 = 0; ks2 < 4; ++ks2) {
+  for (int ks2 = 0; ks2 < BKV / 16; ++ks2) {
     const int dr = lane & 31;
-    vfo[ks2] = KT_U4 * 16 + (dr * 8 + ((ks2 * 2 + hl) ^ ((dr >> 1) & 7))) * 16;
+    vfo[ks2] = KT_U4 * 16 + (dr * VCH + vswz(dr, ks2 * 2 + hl)) * 16;
   }
   auto lds_frag = [&](int byte_off) __attribute__((always_inline)) {
     return __builtin_bit_cast(bf16x8_t, *(const uint4*)(lbase + byte_off));
   };
 
-  // S^T of one 64-key tile: two 32x32 blocks (keys kb*32 + (i/4)*8 + hl*4 + i%4 of
+  // S^T of one key tile: BKV / 32 blocks of 32x32 (keys kb*32 + (i/4)*8 + hl*4 + i%4 of
   // register i, query lane % 32)
   auto scores = [&](auto stc, f32x16_t* s) __attribute__((always_inline)) {
     constexpr int st = decltype(stc)::value;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < BKV / 32; ++kb)
 #pragma unroll
       for (int i = 0; i < 16; ++i) s[kb][i] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < HD / 16; ++ks) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+      for (int kb = 0; kb < BKV / 32; ++kb) {
         // key kb*32 + lane%32 keeps the swizzle term of key lane%32 (kb*32 is a multiple of 16)
         const bf16x8_t u = lds_frag(kfo[ks] + st * STAGE_B + kb * 32 * CH * 16);
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(u, qf[ks], s[kb], 0, 0, 0);
       }
     }
     // keep four fragment reads ahead of the MFMAs that consume them
-    sched_read_ahead<2 * HD / 16, 4>();
+    sched_read_ahead<BKV / 32 * HD / 16, 4>();
   };
   // Probabilities of one tile against the running max m_i, rounded to bf16 in
   // the order the P V operand wants them (key pairs packed by one convert);
@@ -209,7 +229,7 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
     float t0 = 0.f, t1 = 0.f;
     const bf16x2_t one = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
-    for (int x = 0; x < 4; ++x) {
+    for (int x = 0; x < BKV / 16; ++x) {
       uint32_t w[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -237,19 +257,19 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
     const int kv0 = j * BKV;
     if (kv0 + BKV > L) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < BKV / 32; ++kb)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int key = kv0 + kb * 32 + (i >> 2) * 8 + hl * 4 + (i & 3);
           if (key >= L) s[kb][i] = -INFINITY;
         }
     }
-    bf16x8_t pf[4];
+    bf16x8_t pf[BKV / 16];
     float t = exps_pack(s, pf);
     if (__any(!(t <= (float)(1 << (int)RESCALE_SLACK)))) {
       float mx = s[0][0];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < BKV / 32; ++kb)
 #pragma unroll
         for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kb][i]);
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * sl2;
@@ -265,15 +285,15 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
     }
     l_i += t;
 #pragma unroll
-    for (int ks2 = 0; ks2 < 4; ++ks2) {
+    for (int ks2 = 0; ks2 < BKV / 16; ++ks2) {
 #pragma unroll
       for (int db = 0; db < HD / 32; ++db) {
         // d row db*32 + lane%32 keeps the swizzle term of row lane%32
-        const bf16x8_t u = lds_frag(vfo[ks2] + st * STAGE_B + db * 32 * 8 * 16);
+        const bf16x8_t u = lds_frag(vfo[ks2] + st * STAGE_B + db * 32 * VCH * 16);
         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(u, pf[ks2], o[db], 0, 0, 0);
       }
     }
-    sched_read_ahead<4 * HD / 32, 4>();
+    sched_read_ahead<BKV / 16 * HD / 32, 4>();
   };
   // Tile j sits in stage j % 2.  Each tile starts with the loads of tile
   // j + 1 into the other stage (freed by the barrier that ended tile j - 1)
@@ -281,7 +301,7 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
   // wave's part of tile j + 1 is in LDS and no wave reads tile j any more.
   // (A __syncthreads() fence would drain nothing more but costs a wait on
   // every outstanding memory operation.)
-  f32x16_t sc_t[2];
+  f32x16_t sc_t[BKV / 32];
   wait_vmcnt0();
   asm volatile("s_barrier" ::: "memory");
   // The wait before the barrier also covers the LDS reads: the compiler may
@@ -290,20 +310,37 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
   // it by the other waves.
   auto step = [&](int j, auto stc) __attribute__((always_inline)) {
     constexpr int st = decltype(stc)::value;
-    if (j + 1 < ntiles) tile_load(j + 1, std::integral_constant<int, st ^ 1>{});
+    if (j + 1 < je) tile_load(j + 1, std::integral_constant<int, st ^ 1>{});
     scores(stc, sc_t);
     softmax_pv(j, stc, sc_t);
     wait_vmcnt0_lgkmcnt0();
     asm volatile("s_barrier" ::: "memory");
   };
-  int j = 0;
-  for (; j + 1 < ntiles; j += 2) {
+  int j = jb;
+  for (; j + 1 < je; j += 2) {
     step(j, S0{});
     step(j + 1, S1{});
   }
-  if (j < ntiles) step(j, S0{});
+  if (j < je) step(j, S0{});
 
   const float l = l_i + __shfl_xor(l_i, 32, 64);
+  if (a.kv_pieces > 1) {
+    // one key range: O unnormalised, with its max m_i and sum l (every range
+    // holds at least one key, so both are finite), for attn_merge_kernel
+    const long qs = (long)bid * BQ + wave * 32 + (lane & 31);  // query slot
+    float* po = a.split_buf + qs * HD;
+#pragma unroll
+    for (int db = 0; db < HD / 32; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        *(float4*)(po + db * 32 + g * 8 + hl * 4) =
+            make_float4(o[db][g * 4 + 0], o[db][g * 4 + 1], o[db][g * 4 + 2], o[db][g * 4 + 3]);
+    if (hl == 0) {
+      float2* pml = (float2*)(a.split_buf + (long)a.units * a.kv_pieces * BQ * HD);
+      pml[qs] = make_float2(m_i, l);
+    }
+    return;
+  }
   if (qrow < L) {
     const float inv = 1.0f / l;
     const int row = a.o_stream_major ? padded_to_row(a.meta, r, qrow) : a.meta.joint_off[r] + qrow;
@@ -318,6 +355,64 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
         w.y = pack_bf16x2(o[db][g * 4 + 2] * inv, o[db][g * 4 + 3] * inv);
         *(uint2*)(og + dd) = w;
       }
+  }
+}
+
+// Merge of a key-split launch: for each query of unit unit0 + blockIdx.x, the
+// KP key ranges' unnormalised outputs O_p with maxima m_p (log2 domain) and
+// sums l_p combine as O = sum_p 2^(m_p - M) O_p / sum_p 2^(m_p - M) l_p with
+// M = max_p m_p, added in piece order.  Two threads per query, HD / 2
+// dimensions each.
+template <int HD>
+__global__ __launch_bounds__(256) void attn_merge_kernel(const AttnArgs a, const AttnSched sc) {
+  constexpr int BQ = 128;
+  constexpr int DH = HD / 2;
+  const int u = blockIdx.x;
+  const int id = a.unit0 + u;
+  const int per_head = sc.tile_off[sc.n];
+  const int h = id / per_head;
+  const int t = id - h * per_head;
+  int slot = 0;
+  while (slot + 1 < sc.n && t >= sc.tile_off[slot + 1]) ++slot;
+  const int r = sc.req[slot];
+  const int ql = threadIdx.x >> 1, part = threadIdx.x & 1;
+  const int qrow = (t - sc.tile_off[slot]) * BQ + ql;
+  const int L = a.meta.joint_off[r + 1] - a.meta.joint_off[r];
+  if (qrow >= L) return;
+  const int KP = a.kv_pieces, U = a.units;
+  const float2* pml = (const float2*)(a.split_buf + (long)U * KP * BQ * HD);
+  float M = -INFINITY;
+  for (int p = 0; p < KP; ++p) M = fmaxf(M, pml[(long)(p * U + u) * BQ + ql].x);
+  float acc[DH];
+#pragma unroll
+  for (int i = 0; i < DH; ++i) acc[i] = 0.f;
+  float lsum = 0.f;
+  for (int p = 0; p < KP; ++p) {
+    const long qs = (long)(p * U + u) * BQ + ql;
+    const float2 ml = pml[qs];
+    const float w = exp2f(ml.x - M);
+    lsum = fmaf(w, ml.y, lsum);
+    const float4* src = (const float4*)(a.split_buf + qs * HD + part * DH);
+#pragma unroll
+    for (int c = 0; c < DH / 4; ++c) {
+      const float4 v = src[c];
+      acc[4 * c + 0] = fmaf(w, v.x, acc[4 * c + 0]);
+      acc[4 * c + 1] = fmaf(w, v.y, acc[4 * c + 1]);
+      acc[4 * c + 2] = fmaf(w, v.z, acc[4 * c + 2]);
+      acc[4 * c + 3] = fmaf(w, v.w, acc[4 * c + 3]);
+    }
+  }
+  const float inv = 1.0f / lsum;
+  const int row = a.o_stream_major ? padded_to_row(a.meta, r, qrow) : a.meta.joint_off[r] + qrow;
+  bf16_t* og = (bf16_t*)a.o + (long)row * a.o_tok + (long)h * a.o_head + part * DH;
+#pragma unroll
+  for (int c = 0; c < DH / 8; ++c) {
+    uint4 w;
+    w.x = pack_bf16x2(acc[8 * c + 0] * inv, acc[8 * c + 1] * inv);
+    w.y = pack_bf16x2(acc[8 * c + 2] * inv, acc[8 * c + 3] * inv);
+    w.z = pack_bf16x2(acc[8 * c + 4] * inv, acc[8 * c + 5] * inv);
+    w.w = pack_bf16x2(acc[8 * c + 6] * inv, acc[8 * c + 7] * inv);
+    *(uint4*)(og + 8 * c) = w;
   }
 }
 
@@ -473,13 +568,66 @@ AttnSched make_sched(const BatchMeta& m, int bq) {
 
 }  // namespace
 
+// keys per tile of the bf16 kernel; a request's V^T columns are padded to a
+// multiple of kSeqPad, so a tile never reads past them
+constexpr int kKeyTile = 64;
+static_assert(kSeqPad % kKeyTile == 0, "V^T padding");
+
 template <int NW, int HD>
 hipError_t launch_attn_cfg(const AttnArgs& a, hipStream_t s) {
   const AttnSched sc = make_sched(a.meta, NW * 32);
   const long blocks = (long)sc.tile_off[sc.n] * a.heads;
   if (blocks == 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_bf16_kernel<NW, HD, 2>), dim3((unsigned)blocks), dim3(NW * 64), 0, s, a, sc);
+  AttnArgs b = a;
+  b.unit0 = 0;
+  b.units = (int)blocks;
+  b.kv_pieces = 1;
+  hipLaunchKernelGGL((attn_bf16_kernel<NW, HD, 2, kKeyTile>), dim3((unsigned)blocks), dim3(NW * 64), 0, s, b, sc);
   return hipGetLastError();
+}
+
+// Key split of the last round.  A launch of U 128-query units on the 512
+// block slots of the GPU (two per CU) runs floor(U / 512) full rounds and a
+// last one of T = U mod 512 units.  A unit alone on its CU runs about twice
+// as fast as one of a pair, so a last round of up to 256 units costs about
+// what its share of work would; below a quarter round, though, it still
+// costs more (measured on MI355X at 16 384 tokens and head dim 128: 0.25 of
+// a round of units took 0.37 of a round's time, 0.5 took 0.5).  When
+// T <= 128 after R >= 2 full rounds, those T units instead run as T x P
+// blocks of one key range each (P = floor(512 / T) >= 4 pieces, 1/P as long),
+// and a merge kernel combines the pieces.  Measured against the unsplit
+// launch at 16 384-17 152 tokens and 24-25 heads: 1.1-1.7% faster for
+// T = 24-128 (P = 21-4), equal at P = 3 and 1% slower at P = 2, hence the
+// bound.  Requests of one length only (the units of a mixed batch differ in
+// cost), head dim 128.
+struct SplitPlan {
+  int main_units, tail_units, pieces;  // pieces 0: no split
+};
+
+constexpr int kAttnSlots = 2 * 256;  // 128-query blocks resident per GPU (two per CU, 256 CUs)
+
+SplitPlan split_plan(const BatchMeta& m, int heads, int head_dim) {
+  SplitPlan p{0, 0, 0};
+  if (head_dim != 128) return p;
+  const AttnSched sc = make_sched(m, 128);
+  if (sc.n == 0) return p;
+  const int L0 = m.joint_off[sc.req[0] + 1] - m.joint_off[sc.req[0]];
+  for (int i = 1; i < sc.n; ++i)
+    if (m.joint_off[sc.req[i] + 1] - m.joint_off[sc.req[i]] != L0) return p;
+  const long units = (long)sc.tile_off[sc.n] * heads;
+  const long full = units / kAttnSlots, tail = units % kAttnSlots;
+  if (full < 2 || tail == 0 || 4 * tail > kAttnSlots) return p;
+  const int key_tiles = (L0 + kKeyTile - 1) / kKeyTile;
+  const int pieces = (int)std::min<long>(kAttnSlots / tail, key_tiles);
+  if (pieces < 2) return p;
+  p.main_units = (int)(full * kAttnSlots);
+  p.tail_units = (int)tail;
+  p.pieces = pieces;
+  return p;
+}
+
+size_t split_bytes(const SplitPlan& p, int head_dim) {
+  return p.pieces ? (size_t)p.tail_units * p.pieces * 128 * (head_dim + 2) * sizeof(float) : 0;
 }
 
 // Measured on MI355X: software pipelines that overlap a tile's softmax with
@@ -493,9 +641,14 @@ hipError_t launch_attn_cfg(const AttnArgs& a, hipStream_t s) {
 // of two.  Blocks of 256 queries (8 waves, one per CU) read each K/V tile once
 // for twice the queries but get no such lone tail.  So with U units (128
 // queries x heads) on 2 x 256 block slots, the 128-query blocks win when the
-// last round is at most half full (frac(U / 512) <= 1/2) and the 256-query
-// blocks otherwise.  Measured on MI355X (in-process A/B) at 16 896 tokens:
-// 6 heads (U = 792) 256-query blocks -11%, 12 heads (1584) +4%, 18 heads
+// 256-query launch's last round (of 256 slots) is at most half full and the
+// 256-query blocks otherwise: with an even number of 128-query tiles per
+// request that is frac(U / 512) <= 1/2; with an odd number each request
+// adds a half-empty 256-query block (at 19 072 tokens, 24 heads: 1800
+// blocks, a last round of 8; the 128-query blocks are 6% faster there).
+// Measured on MI355X (in-process A/B) at
+// 16 896 tokens: 6 heads (U = 792) 256-query blocks -11%, 12 heads (1584)
+// +4%, 18 heads
 // (2376) -7%, 24 heads (3168) +2%; at 4608 tokens: 24 heads (864) -4%,
 // 48 heads (1728) +3%; whole steps at 256 px (144) +1.8% and 512 px (288)
 // -0.9%.  The rule assumes equal units, i.e. requests of one length; for a
@@ -506,6 +659,22 @@ hipError_t launch_attn_cfg(const AttnArgs& a, hipStream_t s) {
 // launch has 2048 units.
 template <int HD>
 hipError_t launch_attn_hd(const AttnArgs& a, hipStream_t s) {
+  const SplitPlan sp = a.split_buf ? split_plan(a.meta, a.heads, HD) : SplitPlan{0, 0, 0};
+  if (sp.pieces) {
+    const AttnSched sc = make_sched(a.meta, 128);
+    AttnArgs b = a;
+    b.unit0 = 0;
+    b.units = sp.main_units;
+    b.kv_pieces = 1;
+    hipLaunchKernelGGL((attn_bf16_kernel<4, HD, 2, kKeyTile>), dim3((unsigned)sp.main_units), dim3(256), 0, s, b, sc);
+    b.unit0 = sp.main_units;
+    b.units = sp.tail_units;
+    b.kv_pieces = sp.pieces;
+    hipLaunchKernelGGL((attn_bf16_kernel<4, HD, 2, kKeyTile>), dim3((unsigned)(sp.tail_units * sp.pieces)), dim3(256), 0, s, b,
+                       sc);
+    hipLaunchKernelGGL((attn_merge_kernel<HD>), dim3((unsigned)sp.tail_units), dim3(256), 0, s, b, sc);
+    return hipGetLastError();
+  }
   const AttnSched sc4 = make_sched(a.meta, 4 * 32);
   const long units = (long)sc4.tile_off[sc4.n] * a.heads;
   bool wide;
@@ -514,8 +683,12 @@ hipError_t launch_attn_hd(const AttnArgs& a, hipStream_t s) {
     const int L0 = a.meta.joint_off[sc4.req[0] + 1] - a.meta.joint_off[sc4.req[0]];
     for (int i = 1; i < sc4.n; ++i)
       equal = equal && a.meta.joint_off[sc4.req[i] + 1] - a.meta.joint_off[sc4.req[i]] == L0;
-    constexpr long kSlots = 2 * 256;  // 128-query blocks resident per GPU (two per CU, 256 CUs)
-    wide = equal && 2 * (units % kSlots) > kSlots;
+    // fill of the 256-query launch's own last round (its block count is not
+    // units / 2 when a request has an odd number of 128-query tiles)
+    const AttnSched sc8 = make_sched(a.meta, 8 * 32);
+    const long units8 = (long)sc8.tile_off[sc8.n] * a.heads;
+    constexpr long kSlots8 = 256;  // 256-query blocks resident per GPU (one per CU)
+    wide = equal && 2 * (units8 % kSlots8) > kSlots8;
   } else {
     wide = units < 2048;
   }
@@ -527,6 +700,10 @@ hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s) {
   if (a.head_dim == 128) return launch_attn_hd<128>(a, s);
   if (a.head_dim == 64) return launch_attn_hd<64>(a, s);
   return hipErrorInvalidValue;
+}
+
+size_t attn_split_bytes(const BatchMeta& m, int heads, int head_dim) {
+  return split_bytes(split_plan(m, heads, head_dim), head_dim);
 }
 
 hipError_t launch_attention_f32(const AttnArgs& a, hipStream_t s) {

@@ -490,6 +490,10 @@ hipError_t attention(const Ctx& x) {
   a.scale = 1.0f / sqrtf((float)x.L.d);
   for (int r = 0; r <= x.meta.n_req; ++r) a.qk_off[r] = a.vt_off[r] = x.meta.pad_off[r];
   a.meta = x.meta;
+  // the split GEMMs' partial-sum slots double as the attention's key-split
+  // scratch (the two never run at once); null in batch-invariant mode
+  if (x.ws.sk_part && attn_split_bytes(x.meta, a.heads, a.head_dim) <= (size_t)kSplitPartBytes)
+    a.split_buf = x.ws.sk_part;
   return attn_launch(x.s, x.c->dtype, a);
 }
 
@@ -891,6 +895,7 @@ dit_status dit_attention_workspace_size(const dit_batch* batch, int heads, int h
   if (dtype != DIT_F32 && dtype != DIT_BF16) return fail(DIT_ERR_INVALID_ARG, "dtype %d", dtype);
   const BatchMeta m = make_meta(batch);
   *bytes = align256((size_t)heads * head_dim * m.pad_off[m.n_req] * elem_size(dtype));
+  if (dtype == DIT_BF16) *bytes += align256(attn_split_bytes(m, heads, head_dim));
   return DIT_OK;
 }
 
@@ -938,6 +943,8 @@ dit_status dit_attention(const dit_batch* batch, int heads, int head_dim, int dt
     a.vt_off[r] = m.pad_off[r];
   }
   a.meta = m;
+  if (dtype == DIT_BF16 && attn_split_bytes(m, heads, head_dim) > 0)
+    a.split_buf = (float*)((char*)ws + align256((size_t)heads * head_dim * Tp * elem_size(dtype)));
   HIP_TRY(attn_launch(s, dtype, a));
   return DIT_OK;
 }

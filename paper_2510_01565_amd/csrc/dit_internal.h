@@ -175,8 +175,19 @@ struct AttnArgs {
   int qk_off[kMaxReq + 1];
   int vt_off[kMaxReq + 1];
   BatchMeta meta;
+  // Scratch for splitting the key range of a launch's last, partly filled
+  // round of query tiles (bf16, head dim 128): at least
+  // attn_split_bytes(meta, heads, head_dim) bytes, or null (never split; the
+  // output bits then do not depend on how many other tiles share the launch).
+  float* split_buf;
+  // set by the launcher: this launch covers query-tile units
+  // [unit0, unit0 + units); kv_pieces > 1 splits each unit's keys into that
+  // many ranges whose unnormalised partial results go to split_buf
+  int unit0, units, kv_pieces;
 };
 hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s);
+// bytes of split_buf the bf16 launcher may use for this batch (0: it never splits)
+size_t attn_split_bytes(const BatchMeta& m, int heads, int head_dim);
 hipError_t launch_attention_f32(const AttnArgs& a, hipStream_t s);
 
 // elementwise / reduction kernels

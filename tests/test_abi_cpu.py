@@ -104,6 +104,37 @@ def test_split_workspace_only_without_batch_invariance():
         dit.workspace_size(dit.make_config(f32, dit.DIT_FLAG_BATCH_INVARIANT), b)
 
 
+def _split_bytes(tail_units, pieces, d=128):
+    return -(-(tail_units * pieces * 128 * (d + 2) * 4) // 256) * 256
+
+
+def test_attention_key_split_rule():
+    """The bf16 attention splits the key ranges of its last round of
+    128-query tiles only when that round holds at most a quarter of the 512
+    block slots and follows at least two full rounds, every request has one
+    length and the head dim is 128; the extra workspace is the pieces' fp32
+    partials (P = min(512 // T, key tiles) pieces per leftover tile)."""
+    bf = dit.DIT_BF16
+
+    def extra(b, heads, d=128):
+        vt = dit.attention_workspace_size(b, heads, d, dit.DIT_F32) // 2  # same V^T shape, fp32 has no split
+        return dit.attention_workspace_size(b, heads, d, bf) - -(-vt // 256) * 256
+    one = dit.Batch([31], [31], [39])                    # 1000 tokens: 8 query tiles, 16 key tiles
+    assert extra(one, 136) == _split_bytes(64, 8)        # 1088 units: 2 rounds + 64
+    assert extra(one, 144) == _split_bytes(128, 4)       # 1152: 2 rounds + 128
+    assert extra(one, 145) == 0                          # 1160: last round 136 > 128
+    assert extra(one, 160) == 0                          # 1280: last round 256
+    assert extra(one, 128) == 0                          # 1024: no leftover
+    assert extra(one, 72) == 0                           # 576: one full round only
+    assert extra(one, 136, 64) == 0                      # head dim 64
+    two = dit.Batch([20, 20], [25, 25], [0, 0])           # two requests of 500 tokens: 8 key tiles each
+    assert extra(two, 132) == _split_bytes(32, 8)        # 1056 units: P capped by the 8 key tiles
+    mixed = dit.Batch([20, 25], [25, 20], [0, 1])         # 500 and 501 tokens
+    assert extra(mixed, 132) == 0
+    flux2048 = dit.Batch([128], [128], [512])             # 16 896 tokens, 24 heads: 3168 units
+    assert extra(flux2048, 24) == _split_bytes(96, 5)
+
+
 def test_invalid_batches_are_rejected():
     cfg = dit.make_config(workloads.FLUX_FULL)
     assert _err(dit.workspace_size, cfg, dit.Batch([], [], [])) == dit.DIT_ERR_INVALID_ARG

@@ -151,6 +151,45 @@ def test_attention_bf16_large_logits(d, gain):
     assert normwise_err(o.float().cpu().numpy(), ref) < BF16_TOL
 
 
+@pytest.mark.parametrize("grids,n_txt,heads", [
+    ([(31, 31)], [39], 136),          # 1000 tokens, 1088 units: 64 leftover tiles x 8 key ranges, ragged tiles
+    ([(31, 31)], [39], 144),          # 1152 units: 128 leftover tiles x 4 key ranges
+    ([(20, 25), (25, 20)], [0, 0], 132),  # two requests of 500 tokens: 32 x 8 ranges of one key tile each
+])
+def test_attention_bf16_key_split(grids, n_txt, heads):
+    """The launch whose last round of 128-query tiles is at most half full
+    splits those tiles' keys into ranges merged afterwards; every tile,
+    split or not, against the oracle, and the same bits on a second call."""
+    torch = _torch()
+    lens = [gh * gw + nt for (gh, gw), nt in zip(grids, n_txt)]
+    T, d = sum(lens), 128
+    b = dit.Batch([g[0] for g in grids], [g[1] for g in grids], n_txt)
+    assert dit.attention_workspace_size(b, heads, d, dit.DIT_BF16) > 2 * T * heads * d + 4096  # the split applies
+    q = synth.normal(7, "q", (T, heads, d), bf16=True)
+    k = synth.normal(7, "k", (T, heads, d), bf16=True)
+    v = synth.normal(7, "v", (T, heads, d), bf16=True)
+    ref = np.empty((T, heads, d))
+    off = 0
+    for L in lens:
+        sl = slice(off, off + L)
+        ref[sl] = O.attention(q[sl].astype(np.float64), k[sl].astype(np.float64), v[sl].astype(np.float64))
+        off += L
+    wsb = dit.attention_workspace_size(b, heads, d, dit.DIT_BF16)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    qd, kd, vd = (to_dev(x, torch.bfloat16) for x in (q, k, v))
+    outs = []
+    for _ in range(2):
+        o = torch.full((T, heads, d), float("nan"), dtype=torch.bfloat16, device="cuda")
+        dit.dit_attention(b, heads, d, dit.DIT_BF16, qd, kd, vd, o, ws, wsb)
+        torch.cuda.synchronize()
+        outs.append(o)
+    got = outs[0].float().cpu().numpy()
+    assert normwise_err(got, ref) < BF16_TOL
+    # the leftover tiles are the last heads' last query tiles: check those heads alone too
+    assert normwise_err(got[:, -2:], ref[:, -2:]) < BF16_TOL
+    assert torch.equal(outs[0], outs[1])
+
+
 @pytest.mark.parametrize("grids,n_txt", [([(16, 16)], [32]), ([(5, 7), (9, 13)], [3, 17])])
 def test_attention_f32(grids, n_txt):
     got, ref = _attn_case(grids, n_txt, 2, 64, False, 4)
