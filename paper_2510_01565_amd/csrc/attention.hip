@@ -252,10 +252,13 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
   // exceeds 2^RESCALE_SLACK (or overflows, as on the first tile) is the true
   // row max formed, the max raised, O and l rescaled, and the tile redone.
   // O and l always share the max they were computed with, so O / l is exact.
-  auto softmax_pv = [&](int j, auto stc, f32x16_t* s) __attribute__((always_inline)) {
+  // Only a request's last key tile can hold keys past L, and only that tile
+  // is run with masking (a run-time test inside every tile is turned by the
+  // compiler into a compare and select per score on every tile).
+  auto softmax_pv = [&](int j, auto stc, auto maskc, f32x16_t* s) __attribute__((always_inline)) {
     constexpr int st = decltype(stc)::value;
-    const int kv0 = j * BKV;
-    if (kv0 + BKV > L) {
+    if constexpr (decltype(maskc)::value) {
+      const int kv0 = j * BKV;
 #pragma unroll
       for (int kb = 0; kb < BKV / 32; ++kb)
 #pragma unroll
@@ -308,20 +311,28 @@ void attn_bf16_kernel(const AttnArgs a, const AttnSched sc) {
   // place the last P V MFMAs (and the waits for their V^T fragments) after the
   // barrier, and the stage those fragments come from is reloaded right after
   // it by the other waves.
-  auto step = [&](int j, auto stc) __attribute__((always_inline)) {
+  auto step = [&](int j, auto stc, auto maskc) __attribute__((always_inline)) {
     constexpr int st = decltype(stc)::value;
     if (j + 1 < je) tile_load(j + 1, std::integral_constant<int, st ^ 1>{});
     scores(stc, sc_t);
-    softmax_pv(j, stc, sc_t);
+    softmax_pv(j, stc, maskc, sc_t);
     wait_vmcnt0_lgkmcnt0();
     asm volatile("s_barrier" ::: "memory");
   };
+  using NoMask = std::false_type;
+  using Mask = std::true_type;
+  // tiles [jb, jm) hold no key past L; tile jm (if any) is the request's last
+  const int jm = (je == nt_all && L % BKV != 0) ? je - 1 : je;
   int j = jb;
-  for (; j + 1 < je; j += 2) {
-    step(j, S0{});
-    step(j + 1, S1{});
+  for (; j + 1 < jm; j += 2) {
+    step(j, S0{}, NoMask{});
+    step(j + 1, S1{}, NoMask{});
   }
-  if (j < je) step(j, S0{});
+  if (j < jm) step(j++, S0{}, NoMask{});
+  if (j < je) {
+    if (((j - jb) & 1) == 0) step(j, S0{}, Mask{});
+    else step(j, S1{}, Mask{});
+  }
 
   const float l = l_i + __shfl_xor(l_i, 32, 64);
   if (a.kv_pieces > 1) {
