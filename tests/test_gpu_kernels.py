@@ -190,6 +190,34 @@ def test_attention_bf16_key_split(grids, n_txt, heads):
     assert torch.equal(outs[0], outs[1])
 
 
+@pytest.mark.parametrize("gain", [4.0, 16.0])
+def test_attention_bf16_key_split_large_logits(gain):
+    """The key-split merge with scores far outside the unit range: each key
+    range has its own running max, tens to hundreds apart in the log2
+    domain, and the merge rescales the ranges' sums and outputs to the
+    largest (1000 tokens, 136 heads: 64 leftover query tiles x 8 key ranges)."""
+    torch = _torch()
+    grids, n_txt, heads, d = [(31, 31)], [39], 136, 128
+    T = 31 * 31 + 39
+    b = dit.Batch([31], [31], n_txt)
+    q = (synth.normal(8, "q", (T, heads, d)) * gain).astype(np.float32)
+    k = (synth.normal(8, "k", (T, heads, d)) * gain).astype(np.float32)
+    v = synth.normal(8, "v", (T, heads, d), bf16=True)
+    qb = torch.from_numpy(q).to(torch.bfloat16)
+    kb = torch.from_numpy(k).to(torch.bfloat16)
+    ref = O.attention(qb.float().numpy().astype(np.float64), kb.float().numpy().astype(np.float64),
+                      v.astype(np.float64))
+    wsb = dit.attention_workspace_size(b, heads, d, dit.DIT_BF16)
+    assert wsb > 2 * T * heads * d + 4096  # the split applies
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    o = torch.full((T, heads, d), float("nan"), dtype=torch.bfloat16, device="cuda")
+    dit.dit_attention(b, heads, d, dit.DIT_BF16, qb.cuda(), kb.cuda(), to_dev(v, torch.bfloat16), o, ws, wsb)
+    torch.cuda.synchronize()
+    got = o.float().cpu().numpy()
+    assert normwise_err(got, ref) < BF16_TOL
+    assert normwise_err(got[:, -8:], ref[:, -8:]) < BF16_TOL  # the heads whose tiles were split
+
+
 @pytest.mark.parametrize("grids,n_txt", [([(16, 16)], [32]), ([(5, 7), (9, 13)], [3, 17])])
 def test_attention_f32(grids, n_txt):
     got, ref = _attn_case(grids, n_txt, 2, 64, False, 4)
