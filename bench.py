@@ -406,11 +406,12 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="dit57_1024px_bf16")
     ap.add_argument("--extra", default="dit57_256px_bf16,dit57_512px_bf16,dit57_2048px_bf16,"
-                                       "dit57_2048px_sp4_share_bf16,dit57_packed_mixed_bf16,mmdit_double_512px_bf16,"
-                                       "small_block_256px_f32",
+                                       "dit57_2048px_sp4_share_bf16,dit57_packed_mixed_bf16,sd3m_1024px_bf16,"
+                                       "sd3m_512px_bf16,mmdit_double_512px_bf16,small_block_256px_f32",
                     help="comma-separated further workloads reported under per_workload (default: the other "
                          "resolutions of the paper's mix, one GPU's share of the 4-way 2048 px split, the packed "
-                         "mixed-resolution batch, one double block and the small fp32 block; '' for none)")
+                         "mixed-resolution batch, the SD3-Medium-shaped model at 1024 and 512 px, one double "
+                         "block and the small fp32 block; '' for none)")
     ap.add_argument("--extra-steps", type=int, default=10,
                     help="timed steps of each further workload (after --extra-warmup untimed ones)")
     ap.add_argument("--extra-warmup", type=int, default=3)
