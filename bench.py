@@ -402,7 +402,7 @@ def cpu_baseline(wl, seed: int):
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="dit57_1024px_bf16")
     ap.add_argument("--extra", default="dit57_256px_bf16,dit57_512px_bf16,dit57_2048px_bf16,"
@@ -412,7 +412,7 @@ def main() -> int:
                          "resolutions of the paper's mix, one GPU's share of the 4-way 2048 px split, the packed "
                          "mixed-resolution batch, the SD3-Medium-shaped model at 1024 and 512 px, one double "
                          "block and the small fp32 block; '' for none)")
-    ap.add_argument("--extra-steps", type=int, default=10,
+    ap.add_argument("--extra-steps", type=int, default=20,
                     help="timed steps of each further workload (after --extra-warmup untimed ones)")
     ap.add_argument("--extra-warmup", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
@@ -506,6 +506,7 @@ def main() -> int:
                    "text_tokens": wl.n_txt, "requests": len(g), "parallelism": "single GPU"},
         "tflops": main_res["tflops"], "frac_bf16_peak": main_res["frac_peak"],
         "tflop_per_step": main_res["tflop_per_step"], "cv_pct": main_res["cv_pct"],
+        "ms_median_event": main_res["ms_median_event"],
         "roofline": rl, "cpu_baseline": cpu,
         "steps_per_s_by_resolution": {str(workloads.WORKLOADS[n].resolutions[0]): round(r["steps_per_s"], 3)
                                       for n, r in per.items()
