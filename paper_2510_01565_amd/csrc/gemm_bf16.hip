@@ -492,6 +492,17 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
     __syncthreads();
   }
   const bf16_t* bias = (const bf16_t*)E.bias;
+  // The bias of every column this lane stages, loaded before the first output
+  // store: loads and stores share one in-order counter, so a bias load issued
+  // after a column group's stores would wait for them, and the groups would
+  // follow one another at the latency of their stores.
+  constexpr int NBC = DTL ? FN16 : FN;
+  float bcol[NBC];
+#pragma unroll
+  for (int q = 0; q < NBC; ++q) {
+    const int n = n0 + wn * WTN + (DTL ? q * 16 + (lane & 15) : q * 32 + (lane & 31));
+    bcol[q] = (bias != nullptr && n < N) ? bf2f(bias[n]) : 0.f;
+  }
   const int rl = lane >> 1, cseg = (lane & 1) * 16;
   // column groups of 32 (the last one 16 wide when the wave tile is an odd
   // number of 16-column fragments)
@@ -501,8 +512,7 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
     constexpr int NB16 = DTL ? (FN16 - 2 * j < 2 ? FN16 - 2 * j : 2) : 2;  // 16-column blocks in the group
     constexpr int NCOL = 16 * NB16;
     const int nb = n0 + wn * WTN + j * 32;
-    const int nl = nb + (lane & 31);
-    const float bn = (bias != nullptr && nl < N) ? bf2f(bias[nl]) : 0.f;
+    const float bn = DTL ? 0.f : bcol[j];
     // V^T columns of a QKV epilogue: a lane takes one column and 16 consecutive
     // rows, which (when they are 16 consecutive, 16-aligned padded positions of
     // one request) land in one aligned 16-key group of V^T: two 16-byte stores.
@@ -512,8 +522,7 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
       if constexpr (DTL) {
         static_for<NB16>([&](auto bb) {
           constexpr int b = decltype(bb)::value;
-          const int nl16 = nb + b * 16 + (lane & 15);
-          const float bn16 = (bias != nullptr && nl16 < N) ? bf2f(bias[nl16]) : 0.f;
+          const float bn16 = bcol[2 * j + b];
           static_for<2>([&](auto aa) {
             constexpr int a = decltype(aa)::value;
             static_for<4>([&](auto rr) {
