@@ -507,18 +507,20 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
   // column groups of 32 (the last one 16 wide when the wave tile is an odd
   // number of 16-column fragments)
   constexpr int NJ = DTL ? (FN16 + 1) / 2 : FN;
-  static_for<NJ>([&](auto jj) {
-    constexpr int j = decltype(jj)::value;
-    constexpr int NB16 = DTL ? (FN16 - 2 * j < 2 ? FN16 - 2 * j : 2) : 2;  // 16-column blocks in the group
-    constexpr int NCOL = 16 * NB16;
-    const int nb = n0 + wn * WTN + j * 32;
-    const float bn = DTL ? 0.f : bcol[j];
-    // V^T columns of a QKV epilogue: a lane takes one column and 16 consecutive
-    // rows, which (when they are 16 consecutive, 16-aligned padded positions of
-    // one request) land in one aligned 16-key group of V^T: two 16-byte stores.
-    const bool vcols = E.mode == EPI_QKV && nb >= 2 * E.hidden && nb < 3 * E.hidden;
-    static_for<FM>([&](auto ii) {
-      constexpr int i = decltype(ii)::value;
+  // Row groups outer, column groups inner: consecutive stores of a lane fill
+  // adjacent 64-byte pieces of the same rows.
+  static_for<FM>([&](auto ii) {
+    constexpr int i = decltype(ii)::value;
+    static_for<NJ>([&](auto jj) {
+      constexpr int j = decltype(jj)::value;
+      constexpr int NB16 = DTL ? (FN16 - 2 * j < 2 ? FN16 - 2 * j : 2) : 2;  // 16-column blocks in the group
+      constexpr int NCOL = 16 * NB16;
+      const int nb = n0 + wn * WTN + j * 32;
+      const float bn = DTL ? 0.f : bcol[j];
+      // V^T columns of a QKV epilogue: a lane takes one column and 16 consecutive
+      // rows, which (when they are 16 consecutive, 16-aligned padded positions of
+      // one request) land in one aligned 16-key group of V^T: two 16-byte stores.
+      const bool vcols = E.mode == EPI_QKV && nb >= 2 * E.hidden && nb < 3 * E.hidden;
       if constexpr (DTL) {
         static_for<NB16>([&](auto bb) {
           constexpr int b = decltype(bb)::value;
