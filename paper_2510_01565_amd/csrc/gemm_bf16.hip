@@ -507,8 +507,8 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
   // column groups of 32 (the last one 16 wide when the wave tile is an odd
   // number of 16-column fragments)
   constexpr int NJ = DTL ? (FN16 + 1) / 2 : FN;
-  // Row groups outer, column groups inner: consecutive stores of a lane fill
-  // adjacent 64-byte pieces of the same rows.
+  // Row groups outer, column groups inner: a lane's consecutive column groups
+  // write adjacent pieces of the same rows (64 bytes of bf16 output each).
   static_for<FM>([&](auto ii) {
     constexpr int i = decltype(ii)::value;
     static_for<NJ>([&](auto jj) {
