@@ -72,6 +72,27 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+
+// Single instructions as volatile asm statements, which the compiler keeps in
+// the order written: a main loop built from them runs exactly its schedule.
+// The compiler does not see what they do, so the loop that uses them issues
+// its own LDS waits, and wait states separate its last MFMAs from any other
+// reader of the accumulators.
+template <int OFF>
+__device__ __forceinline__ void asm_lds_read16(i32x4_t& d, int addr) {
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(d) : "v"(addr), "i"(OFF));
+}
+__device__ __forceinline__ void asm_mfma16(f32x4_t& c, const i32x4_t& a, const i32x4_t& b) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(c) : "v"(a), "v"(b));
+}
+// wait until at most N LDS operations of this wave are outstanding; none is
+// emitted for N >= 15, since the counter never holds more than 15
+template <int N>
+__device__ __forceinline__ void asm_lgkm_wait() {
+  if constexpr (N < 15) asm volatile("s_waitcnt lgkmcnt(%0)" ::"i"(N));
+}
+
 template <int BM, int BN, int NWM, int NWN, int BK, int STAGES, bool DTL>
 __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProblem P) {
   constexpr int NT = NWM * NWN * 64;
@@ -278,83 +299,164 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
             16, vo, koff, 0, 0);
       }
     };
-    bf16x8_t ha[2][FM2], hb[2][FN2];
-    auto rd = [&](auto stc, auto ksc) __attribute__((always_inline)) {
-      constexpr int st = decltype(stc)::value, ks = decltype(ksc)::value;
-#pragma unroll
-      for (int i = 0; i < FM2; ++i)
-        ha[ks][i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(lbase + fra[ks] + st * A_STAGE + i * 16 * ROWB));
-#pragma unroll
-      for (int j = 0; j < FN2; ++j)
-        hb[ks][j] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(lbase + frb[ks] + st * B_STAGE + j * 16 * ROWB));
-    };
-    // phase h of k-step ks: fragment rows h FM .. (h + 1) FM - 1
-    auto mm = [&](auto ksc, auto hc) __attribute__((always_inline)) {
-      constexpr int ks = decltype(ksc)::value, h = decltype(hc)::value;
-#pragma unroll
-      for (int i = h * FM; i < (h + 1) * FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN2; ++j)
-          acc16[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ha[ks][i], hb[ks][j], acc16[i][j], 0, 0, 0);
-    };
-    // instruction order of a phase: each MFMA followed by its share of R LDS
-    // reads and V buffer loads
-    auto weave = [&](auto rc, auto vc) __attribute__((always_inline)) {
-      constexpr int R = decltype(rc)::value, V = decltype(vc)::value;
-      static_for<NMP>([&](auto mc) {
-        constexpr int m = decltype(mc)::value;
-        constexpr int r = (m + 1) * R / NMP - m * R / NMP, v = (m + 1) * V / NMP - m * V / NMP;
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                           // MFMA
-        if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);      // DS read
-        if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x020, v, 0);      // VMEM read
-      });
-    };
-    constexpr int QH = IPT / 2;
-    using J0 = std::integral_constant<int, 0>;
-    using J1 = std::integral_constant<int, 1>;
-    auto tile = [&](auto stc, int kt) __attribute__((always_inline)) {
-      constexpr int st = decltype(stc)::value;
-      using SN = std::integral_constant<int, st ^ 1>;
-      // phase 0: this tile's k-step 1 fragments
-      rd(stc, J1{});
-      mm(J0{}, J0{});
-      weave(std::integral_constant<int, NR2>{}, J0{});
-      __builtin_amdgcn_sched_barrier(0);
-      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): own reads of this stage done
-      asm volatile("s_barrier" ::: "memory");
-      // phases 1, 2: the loads of tile kt + 2 into this stage
-      load_part(st, min(kt + 2, KT - 1), 0, QH);
-      mm(J0{}, J1{});
-      weave(J0{}, std::integral_constant<int, QH>{});
-      __builtin_amdgcn_sched_barrier(0);
-      load_part(st, min(kt + 2, KT - 1), QH, IPT);
-      mm(J1{}, J0{});
-      weave(J0{}, std::integral_constant<int, IPT - QH>{});
-      __builtin_amdgcn_sched_barrier(0);
-      // tile kt + 1 landed (only the loads of kt + 2 may still be in flight)
+    if constexpr (BM == 256 && BN == 256 && NWAVES == 8) {
+      // 256x256 tiles: the schedule below with every MFMA, fragment read, LDS
+      // wait and barrier an asm statement, so the instructions issue in exactly
+      // this order (1-2.5% faster than the compiler's placement of the same
+      // schedule, bitwise the same results).  Phases of NMP MFMAs:
+      //  P0  k-step 0, fragment rows 0 .. NA/2-1; one read of this tile's
+      //      k-step-1 fragments after each of the first NR MFMAs
+      //      -- lgkmcnt(0), barrier: no wave reads this stage any more
+      //  P1  k-step 0, rows NA/2 ..; loads 0 .. IPT/2-1 of tile kt+2, evenly
+      //  P2  k-step 1, rows 0 .. NA/2-1; the other loads of tile kt+2
+      //      -- vmcnt(IPT), barrier: tile kt+1 visible
+      //  P3  k-step 1, rows NA/2 ..; the next tile's k-step-0 fragment reads
+      // LDS operations complete in order, so before each P0 MFMA the wait
+      // allows every read issued after the P3 read that MFMA needs.
+      constexpr int NA = FM2, NB = FN2, NR = NA + NB, NMP = (NA / 2) * NB;
+      static_assert(NR <= NMP && IPT % 2 == 0 && NMP % (IPT / 2) == 0, "schedule");
+      const int lds0 = (int)(unsigned)(size_t)(__attribute__((address_space(3))) char*)lbase;
+      const int a0 = lds0 + fra[0], a1 = lds0 + fra[1], b0 = lds0 + frb[0], b1 = lds0 + frb[1];
+      i32x4_t fa0[NA], fb0[NB], fa1[NA], fb1[NB];
+      // k-step-0 fragment reads in the order A0, B0 .. B(NB-1), A1 .. A(NA-1)
+      // (the order the first P0 MFMAs need them); k-step 1: A's, then B's
+      auto rd0 = [&](auto stc, auto rc) __attribute__((always_inline)) {
+        constexpr int st = decltype(stc)::value, r = decltype(rc)::value;
+        if constexpr (r == 0) asm_lds_read16<st * A_STAGE>(fa0[0], a0);
+        else if constexpr (r <= NB) asm_lds_read16<st * B_STAGE + (r - 1) * 16 * ROWB>(fb0[r - 1], b0);
+        else asm_lds_read16<st * A_STAGE + (r - NB) * 16 * ROWB>(fa0[r - NB], a0);
+      };
+      auto rd1 = [&](auto stc, auto rc) __attribute__((always_inline)) {
+        constexpr int st = decltype(stc)::value, r = decltype(rc)::value;
+        if constexpr (r < NA) asm_lds_read16<st * A_STAGE + r * 16 * ROWB>(fa1[r], a1);
+        else asm_lds_read16<st * B_STAGE + (r - NA) * 16 * ROWB>(fb1[r - NA], b1);
+      };
+      constexpr int LSTEP = NMP / (IPT / 2);
+      auto tile8 = [&](auto stc, int kt) __attribute__((always_inline)) {
+        constexpr int st = decltype(stc)::value;
+        using SN = std::integral_constant<int, st ^ 1>;
+        const int kt2 = min(kt + 2, KT - 1);
+        static_for<NMP>([&](auto mc) {  // P0: k-step 0, rows 0 .. NA/2-1; this tile's k-step-1 reads
+          constexpr int m = decltype(mc)::value, i = m / NB, j = m % NB;
+          constexpr int ia = i == 0 ? 0 : NB + i, ib = 1 + j;
+          constexpr int need = ia > ib ? ia : ib;
+          asm_lgkm_wait<(NR - 1 - need) + (m < NR ? m : NR)>();
+          asm_mfma16(acc16[i][j], fa0[i], fb0[j]);
+          if constexpr (m < NR) rd1(stc, std::integral_constant<int, m>{});
+        });
+        asm_lgkm_wait<0>();
+        asm volatile("s_barrier" ::: "memory");
+        static_for<NMP>([&](auto mc) {  // P1: k-step 0, rows NA/2 ..; first half of the loads of tile kt+2
+          constexpr int m = decltype(mc)::value, i = NA / 2 + m / NB, j = m % NB;
+          asm_mfma16(acc16[i][j], fa0[i], fb0[j]);
+          if constexpr (m % LSTEP == LSTEP - 1) load_part(st, kt2, m / LSTEP, m / LSTEP + 1);
+        });
+        static_for<NMP>([&](auto mc) {  // P2: k-step 1, rows 0 .. NA/2-1; second half of the loads
+          constexpr int m = decltype(mc)::value, i = m / NB, j = m % NB;
+          asm_mfma16(acc16[i][j], fa1[i], fb1[j]);
+          if constexpr (m % LSTEP == LSTEP - 1) load_part(st, kt2, IPT / 2 + m / LSTEP, IPT / 2 + m / LSTEP + 1);
+        });
+        wait_vmcnt<IPT>();
+        asm volatile("s_barrier" ::: "memory");
+        static_for<NMP>([&](auto mc) {  // P3: k-step 1, rows NA/2 ..; the next tile's k-step-0 reads
+          constexpr int m = decltype(mc)::value, i = NA / 2 + m / NB, j = m % NB;
+          asm_mfma16(acc16[i][j], fa1[i], fb1[j]);
+          if constexpr (m < NR) rd0(SN{}, std::integral_constant<int, m>{});
+        });
+      };
+      load_part(0, 0, 0, IPT);
+      load_part(1, min(1, KT - 1), 0, IPT);
       wait_vmcnt<IPT>();
       asm volatile("s_barrier" ::: "memory");
-      // phase 3: the next tile's k-step 0 fragments
-      rd(SN{}, J0{});
-      mm(J1{}, J1{});
-      weave(std::integral_constant<int, NR2>{}, J0{});
-      __builtin_amdgcn_sched_barrier(0);
-    };
-    // Loads past the last K tile fetch it again into a stage nobody reads any
-    // more (no branches, constant wait counts).  The barriers are bare
-    // s_barriers: a __syncthreads() fence would also drain the loads still in
-    // flight for later tiles.
-    load_part(0, 0, 0, IPT);
-    load_part(1, min(1, KT - 1), 0, IPT);
-    wait_vmcnt<IPT>();
-    asm volatile("s_barrier" ::: "memory");
-    rd(J0{}, J0{});
-    int kt = 0;
-    for (; kt + 1 < KT; kt += 2) {
-      tile(J0{}, kt);
-      tile(J1{}, kt + 1);
+      static_for<NR>([&](auto rc) { rd0(std::integral_constant<int, 0>{}, rc); });
+      int kt = 0;
+      for (; kt + 1 < KT; kt += 2) {
+        tile8(std::integral_constant<int, 0>{}, kt);
+        tile8(std::integral_constant<int, 1>{}, kt + 1);
+      }
+      if (kt < KT) tile8(std::integral_constant<int, 0>{}, kt);
+      asm_lgkm_wait<0>();
+      // wait states between the last asm MFMAs and the accumulators' next reader
+      asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+    } else {
+    bf16x8_t ha[2][FM2], hb[2][FN2];
+      auto rd = [&](auto stc, auto ksc) __attribute__((always_inline)) {
+        constexpr int st = decltype(stc)::value, ks = decltype(ksc)::value;
+  #pragma unroll
+        for (int i = 0; i < FM2; ++i)
+          ha[ks][i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(lbase + fra[ks] + st * A_STAGE + i * 16 * ROWB));
+  #pragma unroll
+        for (int j = 0; j < FN2; ++j)
+          hb[ks][j] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(lbase + frb[ks] + st * B_STAGE + j * 16 * ROWB));
+      };
+      // phase h of k-step ks: fragment rows h FM .. (h + 1) FM - 1
+      auto mm = [&](auto ksc, auto hc) __attribute__((always_inline)) {
+        constexpr int ks = decltype(ksc)::value, h = decltype(hc)::value;
+  #pragma unroll
+        for (int i = h * FM; i < (h + 1) * FM; ++i)
+  #pragma unroll
+          for (int j = 0; j < FN2; ++j)
+            acc16[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ha[ks][i], hb[ks][j], acc16[i][j], 0, 0, 0);
+      };
+      // instruction order of a phase: each MFMA followed by its share of R LDS
+      // reads and V buffer loads
+      auto weave = [&](auto rc, auto vc) __attribute__((always_inline)) {
+        constexpr int R = decltype(rc)::value, V = decltype(vc)::value;
+        static_for<NMP>([&](auto mc) {
+          constexpr int m = decltype(mc)::value;
+          constexpr int r = (m + 1) * R / NMP - m * R / NMP, v = (m + 1) * V / NMP - m * V / NMP;
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                           // MFMA
+          if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);      // DS read
+          if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x020, v, 0);      // VMEM read
+        });
+      };
+      constexpr int QH = IPT / 2;
+      using J0 = std::integral_constant<int, 0>;
+      using J1 = std::integral_constant<int, 1>;
+      auto tile = [&](auto stc, int kt) __attribute__((always_inline)) {
+        constexpr int st = decltype(stc)::value;
+        using SN = std::integral_constant<int, st ^ 1>;
+        // phase 0: this tile's k-step 1 fragments
+        rd(stc, J1{});
+        mm(J0{}, J0{});
+        weave(std::integral_constant<int, NR2>{}, J0{});
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): own reads of this stage done
+        asm volatile("s_barrier" ::: "memory");
+        // phases 1, 2: the loads of tile kt + 2 into this stage
+        load_part(st, min(kt + 2, KT - 1), 0, QH);
+        mm(J0{}, J1{});
+        weave(J0{}, std::integral_constant<int, QH>{});
+        __builtin_amdgcn_sched_barrier(0);
+        load_part(st, min(kt + 2, KT - 1), QH, IPT);
+        mm(J1{}, J0{});
+        weave(J0{}, std::integral_constant<int, IPT - QH>{});
+        __builtin_amdgcn_sched_barrier(0);
+        // tile kt + 1 landed (only the loads of kt + 2 may still be in flight)
+        wait_vmcnt<IPT>();
+        asm volatile("s_barrier" ::: "memory");
+        // phase 3: the next tile's k-step 0 fragments
+        rd(SN{}, J0{});
+        mm(J1{}, J1{});
+        weave(std::integral_constant<int, NR2>{}, J0{});
+        __builtin_amdgcn_sched_barrier(0);
+      };
+      // Loads past the last K tile fetch it again into a stage nobody reads any
+      // more (no branches, constant wait counts).  The barriers are bare
+      // s_barriers: a __syncthreads() fence would also drain the loads still in
+      // flight for later tiles.
+      load_part(0, 0, 0, IPT);
+      load_part(1, min(1, KT - 1), 0, IPT);
+      wait_vmcnt<IPT>();
+      asm volatile("s_barrier" ::: "memory");
+      rd(J0{}, J0{});
+      int kt = 0;
+      for (; kt + 1 < KT; kt += 2) {
+        tile(J0{}, kt);
+        tile(J1{}, kt + 1);
+      }
+      if (kt < KT) tile(J0{}, kt);
     }
-    if (kt < KT) tile(J0{}, kt);
     // the refetches of the last tile must land before the epilogue reuses LDS
     wait_vmcnt<0>();
     __syncthreads();
