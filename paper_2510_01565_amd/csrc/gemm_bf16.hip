@@ -299,22 +299,25 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
             16, vo, koff, 0, 0);
       }
     };
-    if constexpr (BM == 256 && BN == 256 && NWAVES == 8) {
-      // 256x256 tiles: the schedule below with every MFMA, fragment read, LDS
-      // wait and barrier an asm statement, so the instructions issue in exactly
-      // this order (1-2.5% faster than the compiler's placement of the same
-      // schedule, bitwise the same results).  Phases of NMP MFMAs:
+    if constexpr (FM2 + FN2 <= FM * FN2) {
+      // Every configuration whose phase holds at least one MFMA per fragment
+      // read (all but the 128x64 skinny tile): the schedule below with every
+      // MFMA, fragment read, LDS wait and barrier an asm statement, so the
+      // instructions issue in exactly this order (0.5-2.5% faster than the
+      // compiler's placement of the same schedule, bitwise the same results).
+      // Phases of NMP MFMAs:
       //  P0  k-step 0, fragment rows 0 .. NA/2-1; one read of this tile's
       //      k-step-1 fragments after each of the first NR MFMAs
       //      -- lgkmcnt(0), barrier: no wave reads this stage any more
-      //  P1  k-step 0, rows NA/2 ..; loads 0 .. IPT/2-1 of tile kt+2, evenly
-      //  P2  k-step 1, rows 0 .. NA/2-1; the other loads of tile kt+2
+      //  P1  k-step 0, rows NA/2 ..; loads 0 .. Q1-1 of tile kt+2 spread over it
+      //  P2  k-step 1, rows 0 .. NA/2-1; the other IPT - Q1 loads
+      //  P3  k-step 1, rows NA/2 ..: NMP - NR MFMAs, then
       //      -- vmcnt(IPT), barrier: tile kt+1 visible
-      //  P3  k-step 1, rows NA/2 ..; the next tile's k-step-0 fragment reads
+      //      the rest, each followed by one of the next tile's k-step-0 reads
       // LDS operations complete in order, so before each P0 MFMA the wait
       // allows every read issued after the P3 read that MFMA needs.
       constexpr int NA = FM2, NB = FN2, NR = NA + NB, NMP = (NA / 2) * NB;
-      static_assert(NR <= NMP && IPT % 2 == 0 && NMP % (IPT / 2) == 0, "schedule");
+      static_assert(NR <= NMP, "schedule");
       const int lds0 = (int)(unsigned)(size_t)(__attribute__((address_space(3))) char*)lbase;
       const int a0 = lds0 + fra[0], a1 = lds0 + fra[1], b0 = lds0 + frb[0], b1 = lds0 + frb[1];
       i32x4_t fa0[NA], fb0[NB], fa1[NA], fb1[NB];
@@ -331,7 +334,8 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
         if constexpr (r < NA) asm_lds_read16<st * A_STAGE + r * 16 * ROWB>(fa1[r], a1);
         else asm_lds_read16<st * B_STAGE + (r - NA) * 16 * ROWB>(fb1[r - NA], b1);
       };
-      constexpr int LSTEP = NMP / (IPT / 2);
+      // loads [Q1) of a tile in P1 and [Q1, IPT) in P2, spread evenly over each phase's MFMAs
+      constexpr int Q1 = (IPT + 1) / 2, Q2 = IPT - Q1;
       auto tile8 = [&](auto stc, int kt) __attribute__((always_inline)) {
         constexpr int st = decltype(stc)::value;
         using SN = std::integral_constant<int, st ^ 1>;
@@ -349,19 +353,23 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
         static_for<NMP>([&](auto mc) {  // P1: k-step 0, rows NA/2 ..; first half of the loads of tile kt+2
           constexpr int m = decltype(mc)::value, i = NA / 2 + m / NB, j = m % NB;
           asm_mfma16(acc16[i][j], fa0[i], fb0[j]);
-          if constexpr (m % LSTEP == LSTEP - 1) load_part(st, kt2, m / LSTEP, m / LSTEP + 1);
+          constexpr int q0 = m * Q1 / NMP, q1 = (m + 1) * Q1 / NMP;
+          if constexpr (q1 > q0) load_part(st, kt2, q0, q1);
         });
         static_for<NMP>([&](auto mc) {  // P2: k-step 1, rows 0 .. NA/2-1; second half of the loads
           constexpr int m = decltype(mc)::value, i = m / NB, j = m % NB;
           asm_mfma16(acc16[i][j], fa1[i], fb1[j]);
-          if constexpr (m % LSTEP == LSTEP - 1) load_part(st, kt2, IPT / 2 + m / LSTEP, IPT / 2 + m / LSTEP + 1);
+          constexpr int q0 = m * Q2 / NMP, q1 = (m + 1) * Q2 / NMP;
+          if constexpr (q1 > q0) load_part(st, kt2, Q1 + q0, Q1 + q1);
         });
-        wait_vmcnt<IPT>();
-        asm volatile("s_barrier" ::: "memory");
         static_for<NMP>([&](auto mc) {  // P3: k-step 1, rows NA/2 ..; the next tile's k-step-0 reads
           constexpr int m = decltype(mc)::value, i = NA / 2 + m / NB, j = m % NB;
+          if constexpr (m == NMP - NR) {  // the MFMAs before it need no LDS
+            wait_vmcnt<IPT>();
+            asm volatile("s_barrier" ::: "memory");
+          }
           asm_mfma16(acc16[i][j], fa1[i], fb1[j]);
-          if constexpr (m < NR) rd0(SN{}, std::integral_constant<int, m>{});
+          if constexpr (m >= NMP - NR) rd0(SN{}, std::integral_constant<int, m - (NMP - NR)>{});
         });
       };
       load_part(0, 0, 0, IPT);
