@@ -372,6 +372,14 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
           if constexpr (m >= NMP - NR) rd0(SN{}, std::integral_constant<int, m - (NMP - NR)>{});
         });
       };
+      // The zeroed accumulators pass through an empty asm statement here, so
+      // their initialisation is issued before the prologue and not next to
+      // the first asm MFMA (a VALU write just before an MFMA that reads it
+      // needs wait states the compiler does not know to insert).
+#pragma unroll
+      for (int i = 0; i < NA; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j) asm volatile("" : "+v"(acc16[i][j]));
       load_part(0, 0, 0, IPT);
       load_part(1, min(1, KT - 1), 0, IPT);
       wait_vmcnt<IPT>();
@@ -384,8 +392,14 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
       }
       if (kt < KT) tile8(std::integral_constant<int, 0>{}, kt);
       asm_lgkm_wait<0>();
-      // wait states between the last asm MFMAs and the accumulators' next reader
+      // wait states between the last asm MFMAs and the accumulators' next
+      // reader; each accumulator then passes through an empty asm statement,
+      // which keeps every read of it after the wait states
       asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+#pragma unroll
+      for (int i = 0; i < NA; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j) asm volatile("" : "+v"(acc16[i][j]));
     } else {
     bf16x8_t ha[2][FM2], hb[2][FN2];
       auto rd = [&](auto stc, auto ksc) __attribute__((always_inline)) {
