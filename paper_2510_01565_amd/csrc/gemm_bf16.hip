@@ -223,10 +223,10 @@ __global__ __launch_bounds__(NWM* NWN * 64) void gemm_bf16_kernel(const GemmProb
     // FM x 2FN MFMAs.  Fragment registers hold one whole K tile.  Tile X is
     // read in the last phase of X-1 (k-step 0) and the first phase of X
     // (k-step 1); a barrier after X's first phase frees X's stage and the
-    // loads of tile X+2 into it leave over phases 1 and 2 (one per two MFMAs,
-    // about what the texture path drains); a second barrier before the last
-    // phase makes tile X+1 visible.  A load thus has about one K tile between
-    // its issue and the barrier that needs it.
+    // loads of tile X+2 into it are spread over phases 1 and 2; a second
+    // barrier, in the last phase ahead of its fragment reads, makes tile X+1
+    // visible.  A load thus has about one K tile between its issue and the
+    // barrier that needs it.
     static_assert(BK == 64 && STAGES == 2, "schedule for 64-wide K tiles, two stages");
     constexpr int RPI = 64 / CPR;                       // tile rows per instruction
     constexpr int AI = BM / RPI / NWAVES, BI = BN / RPI / NWAVES;
